@@ -1,0 +1,203 @@
+"""Benchmark of the CHAOS hot path on one MI355X.
+
+One step = one Training epoch of the large net (conv20 k4 -> max2 -> conv60 k3
+-> conv100 k6 -> max2 -> FC150 -> FC10) over the 60,000-sample synthetic set,
+Hogwild with the maximum number of resident workers, lr 1e-3: every sample is
+claimed, forward-propagated, back-propagated and pushed to the shared weights
+layer by layer.  Inputs are resident in HBM before the timed region.
+
+Prints one JSON line.  Extra fields:
+  roofline      the training kernel's algorithmic FLOP rate (dense count of
+                forward, backward-data, weight-gradient and update
+                multiply-adds, x2) over its average launch time, against the
+                MI355X FP32 peak
+  cpu_baseline  the CPU oracle (sequential per-sample SGD, one core) on a
+                bounded sample of the same workload
+  rows          throughput of the frozen-weight 16,384-sample batch gradient
+                and of the 10,000-sample test forward pass
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "training samples/sec (fwd+bwd+update) and % FP32 peak, large net"
+PEAK_FP32_TFLOPS = 157.3
+PROFILE_TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def train_flops_per_sample(layers, in_hw=29):
+    """Dense algorithmic FLOPs of one training sample: 2 x (forward MACs +
+    backward-data MACs of every layer above the input + weight-gradient MACs
+    incl. the bias sums + one multiply-add per parameter for the update)."""
+    c, h, w = 1, in_hw, in_hw
+    fwd = bwd = wgrad = params = 0
+    for i, (kind, maps, k) in enumerate(layers):
+        if kind == 1:
+            ho, wo = h - k + 1, w - k + 1
+            mac = maps * ho * wo * c * k * k
+            fwd += mac
+            if i > 0:
+                bwd += mac
+            wgrad += mac + maps * ho * wo
+            params += maps * (c * k * k + 1)
+            c, h, w = maps, ho, wo
+        elif kind == 2:
+            h, w = h // k, w // k
+        else:
+            s = c * h * w
+            fwd += maps * s
+            if i > 0:
+                bwd += maps * s
+            wgrad += maps * s + maps
+            params += maps * (s + 1)
+            c, h, w = maps, 1, 1
+    return 2 * (fwd + bwd + wgrad + params), 2 * fwd
+
+
+def cpu_baseline(layers, p0, x, y, budget_s=15.0):
+    """The oracle, as it stands, on the first samples of the same set."""
+    from oracle import oracle as orc
+    n = 8
+    t0 = time.perf_counter()
+    orc.train_sequential(layers, p0, x[:n], y[:n], 1e-3)
+    per = (time.perf_counter() - t0) / n
+    n = max(8, min(len(y), int(budget_s / max(per, 1e-6))))
+    t0 = time.perf_counter()
+    orc.train_sequential(layers, p0, x[:n], y[:n], 1e-3)
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "training samples/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} samples of the 60,000-sample training set, sequential "
+                      f"per-sample SGD (fp64 oracle, one thread), {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--net", default="large")
+    ap.add_argument("--workers", type=int, default=0)
+    ap.add_argument("--mode", default="atomic", choices=["atomic", "racy", "sequential"])
+    ap.add_argument("--samples", type=int, default=60000)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-rows", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the path shards by samples across GPUs, see the design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_1506_09067_amd import chaos, workloads as wl
+
+    torch.cuda.set_device(0)
+    layers = wl.NETS[args.net]
+    p0 = wl.init_params(layers)
+    x, y = wl.train_set(args.samples)
+    xd = torch.from_numpy(x).cuda()
+    yd = torch.from_numpy(y).cuda()
+    net = chaos.Net(layers, p0)
+    mode = {"atomic": chaos.HOGWILD_ATOMIC, "racy": chaos.HOGWILD_RACY,
+            "sequential": chaos.SEQUENTIAL}[args.mode]
+    workers = args.workers or net.max_workers
+    if mode == chaos.SEQUENTIAL:
+        workers = 1
+    flops, fwd_flops = train_flops_per_sample(layers)
+
+    for _ in range(args.warmup):
+        net.train_epoch(xd, yd, 1e-3, mode=mode, workers=workers)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        ev[s][0].record(stream)
+        net.train_epoch(xd, yd, 1e-3, mode=mode, workers=workers)
+        ev[s][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    launch_ms = [a.elapsed_time(b) for a, b in ev]
+    total_ms = sum(launch_ms)
+    value = args.samples * args.steps / (total_ms / 1e3)
+    avg_launch_s = total_ms / 1e3 / args.steps
+    achieved = flops * args.samples / avg_launch_s / 1e12
+    traffic = None
+    if os.path.exists(PROFILE_TRAFFIC):
+        with open(PROFILE_TRAFFIC) as f:
+            t = json.load(f)
+        if t.get("net") == args.net and t.get("workers") == workers:
+            traffic = t.get("bytes_per_launch")
+    w = net.get_params()
+    torch.cuda.synchronize()
+    finite = bool(torch.isfinite(w).all().item())
+
+    rows = None
+    if not args.no_rows:
+        rows = {}
+        xb, yb = wl.batch_set(16384)
+        xbd, ybd = torch.from_numpy(xb).cuda(), torch.from_numpy(yb).cuda()
+        g = torch.empty(net.n_params, device="cuda")
+        net.forward_backward(xbd, ybd, grad_sum=g)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        net.forward_backward(xbd, ybd, grad_sum=g)
+        b.record(stream)
+        torch.cuda.synchronize()
+        rows["batch_gradient_16384"] = {"samples_per_s": 16384 / (a.elapsed_time(b) / 1e3),
+                                        "ms": a.elapsed_time(b)}
+        xt, yt = wl.test_set(10000)
+        xtd, ytd = torch.from_numpy(xt).cuda(), torch.from_numpy(yt).cuda()
+        net.evaluate(xtd, ytd)
+        torch.cuda.synchronize()
+        a.record(stream)
+        wrong = net.evaluate(xtd, ytd)
+        b.record(stream)
+        torch.cuda.synchronize()
+        rows["test_forward_10000"] = {"samples_per_s": 10000 / (a.elapsed_time(b) / 1e3),
+                                      "ms": a.elapsed_time(b),
+                                      "tflops": fwd_flops * 10000 / (a.elapsed_time(b) / 1e3) / 1e12,
+                                      "n_wrong": int(wrong.item())}
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(layers, p0, x, y)
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "training samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"CHAOS Training epoch, {args.net} net, {args.samples} synthetic "
+                               f"29x29 samples, Hogwild ({args.mode}) with {workers} workers, lr 1e-3",
+                   "net": args.net, "samples_per_step": args.samples, "workers": workers,
+                   "mode": args.mode, "params": net.n_params,
+                   "train_flop_per_sample": flops},
+        "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_FP32_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_TFLOPS, "traffic": traffic},
+        "cpu_baseline": cpu,
+        "rows": rows,
+        "wall_s": wall,
+        "weights_finite": finite,
+        "launch_ms": launch_ms,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

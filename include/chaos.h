@@ -1,0 +1,148 @@
+/*
+ * chaos.h -- C ABI of libchaos.so, the MI355X (gfx950) implementation of the
+ * CHAOS per-sample back-propagation hot path (Controlled Hogwild with
+ * Arbitrary Order of Synchronization; Viebke & Pllana, HPCC 2015).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every function returns an int status: CHAOS_OK (0) or a negative code.
+ *    Nothing aborts or throws.  chaos_last_error() gives a message for the
+ *    last failing call of the calling thread.
+ *  - Argument and shape errors are detected on the host and returned before
+ *    any work is enqueued.  Launch failures are reported as CHAOS_EDEVICE.
+ *  - Pointers named *_dev are device pointers (hipMalloc'd or torch CUDA
+ *    tensors) owned by the caller; *_host are host pointers.  All device
+ *    work is enqueued on `stream` and is asynchronous: the caller
+ *    synchronises (hipStreamSynchronize / torch.cuda.synchronize) before it
+ *    reads results.  stream = NULL means the null stream.
+ *  - One call at a time per chaos_net; different nets are independent.
+ *  - Images are fp32, row-major [n][in_h * in_w]; labels int32 in
+ *    [0, n_classes) where n_classes is the output size of the last layer.
+ *  - Canonical parameter layout (get/set, init, gradients): layers in order;
+ *    conv: W[o][i][u][v] row-major then b[o]; fully connected: W[j][i] (i over
+ *    the map-major flattened input) then b[j]; pooling layers hold nothing.
+ */
+#ifndef CHAOS_H
+#define CHAOS_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    CHAOS_OK = 0,
+    CHAOS_EINVAL = -1,      /* null pointer, n < 0, unknown kind/mode, bad label range  */
+    CHAOS_ESHAPE = -2,      /* kernel > map, pool not dividing the map, n_params mismatch */
+    CHAOS_ENOMEM = -3,      /* device or host allocation failed                          */
+    CHAOS_EDEVICE = -4,     /* a HIP runtime error; text in chaos_last_error()            */
+    CHAOS_EUNSUPPORTED = -5 /* a shape beyond the library's limits                      */
+};
+
+/* Layer kinds (Section II-A, Table I). */
+enum { CHAOS_CONV = 1, CHAOS_MAXPOOL = 2, CHAOS_FC = 3 };
+
+/* One layer of the architecture (Table I rows).
+ *   CHAOS_CONV:    maps output maps, kernel x kernel weights per (output map,
+ *                  input map) pair, valid cross-correlation, stride 1, every
+ *                  output map connected to every input map, one bias per map.
+ *   CHAOS_MAXPOOL: non-overlapping kernel x kernel max (stride = kernel; the
+ *                  kernel must divide the map); maps is ignored; kernel 1 is
+ *                  the identity.
+ *   CHAOS_FC:      maps neurons, each connected to every input value, one bias.
+ * Every conv and FC layer, the output layer included, applies the activation
+ * f(z) = 1.7159 tanh(2z/3).  The first layer reads the image directly. */
+typedef struct {
+    int32_t kind;
+    int32_t maps;
+    int32_t kernel;
+} chaos_layer;
+
+/* Training modes of chaos_train_epoch (Section III-A).
+ *   CHAOS_SEQUENTIAL      one worker, samples in index order: per-sample SGD.
+ *   CHAOS_HOGWILD_ATOMIC  `workers` concurrent workers claim samples from a
+ *                         shared counter (dynamic work-sharing, III-A.1) and
+ *                         add their per-layer updates to the shared weights
+ *                         with atomic fp32 adds (III-A.2, III-A.3).
+ *   CHAOS_HOGWILD_RACY    as above, but each update is a plain load, fma and
+ *                         store: concurrent updates to one weight may be lost. */
+enum { CHAOS_SEQUENTIAL = 0, CHAOS_HOGWILD_ATOMIC = 1, CHAOS_HOGWILD_RACY = 2 };
+
+typedef struct chaos_net chaos_net; /* opaque; owned by the library */
+
+/* Build a net (Section II-A, Table I): walks the layer list from a 1 x in_h x
+ * in_w input, allocates the shared weights on the current device and copies
+ * init_params_host (n_params floats, canonical layout) into them.
+ * n_params must equal the architecture's weight count (Table I "Weights"
+ * summed over layers), else CHAOS_ESHAPE.  *out receives the handle. */
+int chaos_create_net(int32_t in_h, int32_t in_w, const chaos_layer *layers, int32_t n_layers,
+                     const float *init_params_host, int64_t n_params, chaos_net **out);
+
+/* Free the net and every device buffer it owns.  NULL is accepted. */
+int chaos_destroy_net(chaos_net *net);
+
+/* Number of weights incl. biases (the Table I total), or a negative code. */
+int64_t chaos_num_params(const chaos_net *net);
+
+/* Output size of the last layer (the class count), or a negative code. */
+int32_t chaos_num_outputs(const chaos_net *net);
+
+/* Copy the shared weights to / from a device buffer of chaos_num_params()
+ * floats in the canonical layout, on `stream`. */
+int chaos_get_params(const chaos_net *net, float *dst_dev, hipStream_t stream);
+int chaos_set_params(chaos_net *net, const float *src_dev, hipStream_t stream);
+
+/* Frozen-weight forward and back-propagation of n samples (Section II-A):
+ * the weights are not modified.  Optional outputs, NULL = skip:
+ *   out_dev        [n][n_classes]  last-layer outputs y
+ *   loss_dev       [n]             E_i = 1/2 sum_k (y_k - t_k)^2, t one-hot
+ *   grad_sum_dev   [n_params]      sum_i dE_i/dW, accumulated in a fixed
+ *                                  order: bitwise reproducible run to run
+ *   grad_each_dev  [n][n_params]   per-sample gradients
+ * n = 0 writes zeros into grad_sum_dev and nothing else. */
+int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *labels_dev,
+                           int64_t n, float *out_dev, float *loss_dev, float *grad_sum_dev,
+                           float *grad_each_dev, hipStream_t stream);
+
+/* W <- W - lr * grad_dev (n_params floats, canonical layout). */
+int chaos_apply_update(chaos_net *net, const float *grad_dev, float lr, hipStream_t stream);
+
+/* One Training pass over x[0..n) (Section III-A.1 "Training"): each worker
+ * repeatedly claims the next unprocessed sample (in index order), forward-
+ * propagates it, computes the error against its label and back-propagates;
+ * after each layer's gradients and the partial derivatives below it are
+ * computed, that layer's shared weights receive W <- W - lr * g (Controlled
+ * Hogwild, III-A.2) with no synchronisation between workers (Arbitrary Order
+ * of Synchronization, III-A.3).  workers: number of concurrent workers for
+ * the Hogwild modes (0 = chaos_max_workers(net)); ignored by
+ * CHAOS_SEQUENTIAL.  Values above chaos_max_workers() are CHAOS_EINVAL.
+ * loss_dev [n] (optional): each sample's loss at the time it was processed. */
+int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_dev, int64_t n,
+                      float lr, int32_t mode, int32_t workers, float *loss_dev,
+                      hipStream_t stream);
+
+/* Validation / Testing (Section III-A.1, Table II): forward only.
+ * out_dev [n][n_classes] optional; n_wrong_dev [1] receives the number of
+ * samples whose predicted class (lowest index among maximal outputs) differs
+ * from the label (it is overwritten, not accumulated). */
+int chaos_evaluate(chaos_net *net, const float *x_dev, const int32_t *labels_dev, int64_t n,
+                   float *out_dev, int32_t *n_wrong_dev, hipStream_t stream);
+
+/* Largest number of concurrent Hogwild workers the device keeps resident. */
+int32_t chaos_max_workers(const chaos_net *net);
+
+/* Debug aid: when claims_dev (int32 [n] of the next chaos_train_epoch) is not
+ * NULL, every processed sample index i adds 1 to claims_dev[i]; NULL turns it
+ * off.  The buffer must hold at least n entries for each later call. */
+int chaos_set_claim_counter(chaos_net *net, int32_t *claims_dev);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char *chaos_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CHAOS_H */

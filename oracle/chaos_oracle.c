@@ -433,10 +433,12 @@ int orc_forward_backward(int in_h, int in_w, const int *layers, int n_layers, in
 /* Sequential per-sample SGD over x[0..n) in index order: for each sample a
  * forward pass, the loss, then back-propagation with the per-layer update
  * w <- w - lr * g.  params is updated in place; loss_out[i] (optional) is the
- * loss of sample i before its update. */
+ * loss of sample i before its update, gap_out[i] (optional) the smallest
+ * positive relative max-pool gap of its forward pass. */
 int orc_train_sequential(int in_h, int in_w, const int *layers, int n_layers, int act,
                          double *params, long long n_params, int store_f32, const float *x,
-                         const int *labels, long long n, double lr, double *loss_out)
+                         const int *labels, long long n, double lr, double *loss_out,
+                         double *gap_out)
 {
     orc_net net;
     int rc = build_net(in_h, in_w, layers, n_layers, &net);
@@ -447,9 +449,11 @@ int orc_train_sequential(int in_h, int in_w, const int *layers, int n_layers, in
     orc_ws ws;
     if ((rc = ws_alloc(&net, &ws))) return rc;
     for (long long i = 0; i < n; ++i) {
-        forward(&net, act, params, x + i * net.in_size, &ws, NULL);
+        double gap = INFINITY;
+        forward(&net, act, params, x + i * net.in_size, &ws, &gap);
         double E = loss_and_top_error(&net, &ws, labels[i], ws.e0);
         if (loss_out) loss_out[i] = E;
+        if (gap_out) gap_out[i] = gap;
         backward(&net, act, params, lr, store_f32, &ws, NULL);
     }
     ws_free(&ws);

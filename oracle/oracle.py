@@ -54,7 +54,7 @@ def lib():
         L.orc_conv_backdata.argtypes = [P, i32, i32, P, i32, i32, i32, P]
         L.orc_conv_backdata.restype = None
         L.orc_forward_backward.argtypes = [i32, i32, P, i32, i32, P, i64, P, i32, P, P, P, P]
-        L.orc_train_sequential.argtypes = [i32, i32, P, i32, i32, P, i64, i32, P, P, i64, f64, P]
+        L.orc_train_sequential.argtypes = [i32, i32, P, i32, i32, P, i64, i32, P, P, i64, f64, P, P]
         L.orc_grad_sum.argtypes = [i32, i32, P, i32, i32, P, i64, P, P, i64, P, P]
         L.orc_evaluate.argtypes = [i32, i32, P, i32, i32, P, i64, P, P, i64, P, P]
         for name in ("orc_shape", "orc_forward_backward", "orc_train_sequential",
@@ -158,19 +158,20 @@ def forward_backward(layers, params, x, label, act=ACT_TANH, in_h=29, in_w=29, g
 
 
 def train_sequential(layers, params, x, labels, lr, act=ACT_TANH, store_f32=True,
-                     in_h=29, in_w=29):
-    """Per-sample SGD in index order -> (params after, per-sample losses)."""
+                     in_h=29, in_w=29, with_gaps=False):
+    """Per-sample SGD in index order -> (params after, per-sample losses[, gaps])."""
     ly = _layers(layers)
     p = _params(params).copy()
     x = np.ascontiguousarray(x, dtype=np.float32)
     labels = np.ascontiguousarray(labels, dtype=np.int32)
     n = len(labels)
     losses = np.zeros(n)
+    gaps = np.zeros(n)
     rc = lib().orc_train_sequential(in_h, in_w, _ptr(ly), len(ly) // 3, act, _ptr(p), p.size,
                                     int(store_f32), _ptr(x), _ptr(labels), n, float(lr),
-                                    _ptr(losses))
+                                    _ptr(losses), _ptr(gaps))
     _check(rc, "train_sequential")
-    return p, losses
+    return (p, losses, gaps) if with_gaps else (p, losses)
 
 
 def grad_sum(layers, params, x, labels, act=ACT_TANH, in_h=29, in_w=29):

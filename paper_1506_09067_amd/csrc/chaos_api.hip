@@ -1,0 +1,363 @@
+// Host side of libchaos.so: argument validation, the shape walk of Table I,
+// device memory owned by a net, and the launches behind every entry point
+// declared in include/chaos.h.
+#include "../../include/chaos.h"
+#include "chaos_internal.h"
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+using chaos::Layer;
+using chaos::Net;
+
+struct chaos_net {
+    int device = 0;
+    Net desc{};
+    int64_t n_params = 0;
+    float *params = nullptr;      // shared weights, canonical layout
+    int block = 256;              // threads per worker
+    int max_workers = 0;          // resident workers of the training kernel
+    float *scratch = nullptr;     // [max_workers][scratch_floats]
+    int32_t *counter = nullptr;   // sample claim counter
+    int fb_workers = 0;           // rows of grad_part
+    float *grad_part = nullptr;   // [fb_workers][n_params]
+    int32_t *claims = nullptr;    // debug claim counter (caller-owned)
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+int ok() {
+    g_last_error.clear();
+    return CHAOS_OK;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(CHAOS_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                                     \
+    do {                                                        \
+        hipError_t e_ = (expr);                                 \
+        if (e_ != hipSuccess) return hip_fail(e_, what);        \
+    } while (0)
+
+constexpr int64_t kIntLimit = (int64_t)1 << 30;  // every per-net size must fit int32
+
+// Shape walk (Section II-A, Table I) and per-worker scratch layout.
+int build_desc(int32_t in_h, int32_t in_w, const chaos_layer *layers, int32_t n_layers, Net &net) {
+    if (!layers) return fail(CHAOS_EINVAL, "layers is NULL");
+    if (n_layers < 1 || n_layers > chaos::kMaxLayers)
+        return fail(CHAOS_EINVAL, "n_layers=%d outside [1,%d]", n_layers, chaos::kMaxLayers);
+    if (in_h < 1 || in_w < 1) return fail(CHAOS_EINVAL, "input %dx%d", in_h, in_w);
+    std::memset(&net, 0, sizeof(net));
+    int64_t c = 1, h = in_h, w = in_w, off = 0, scr = 0, emax = (int64_t)in_h * in_w;
+    for (int l = 0; l < n_layers; ++l) {
+        const chaos_layer &src = layers[l];
+        Layer &ly = net.L[l];
+        ly.kind = src.kind;
+        ly.k = src.kernel;
+        ly.cin = (int)c; ly.hin = (int)h; ly.win = (int)w;
+        int64_t nw = 0, nb = 0;
+        if (src.kind == CHAOS_CONV) {
+            if (src.maps < 1 || src.kernel < 1)
+                return fail(CHAOS_EINVAL, "layer %d: conv maps=%d kernel=%d", l, src.maps, src.kernel);
+            if (src.kernel > h || src.kernel > w)
+                return fail(CHAOS_ESHAPE, "layer %d: kernel %d larger than the %lldx%lld map", l,
+                            src.kernel, (long long)h, (long long)w);
+            ly.cout = src.maps;
+            ly.hout = (int)(h - src.kernel + 1);
+            ly.wout = (int)(w - src.kernel + 1);
+            nw = (int64_t)src.maps * c * src.kernel * src.kernel;
+            nb = src.maps;
+        } else if (src.kind == CHAOS_MAXPOOL) {
+            if (src.kernel < 1) return fail(CHAOS_EINVAL, "layer %d: pool kernel %d", l, src.kernel);
+            if (h % src.kernel || w % src.kernel)
+                return fail(CHAOS_ESHAPE, "layer %d: pool %d does not divide the %lldx%lld map", l,
+                            src.kernel, (long long)h, (long long)w);
+            ly.cout = (int)c;
+            ly.hout = (int)(h / src.kernel);
+            ly.wout = (int)(w / src.kernel);
+        } else if (src.kind == CHAOS_FC) {
+            if (src.maps < 1) return fail(CHAOS_EINVAL, "layer %d: fc neurons=%d", l, src.maps);
+            ly.cin = (int)(c * h * w); ly.hin = 1; ly.win = 1;
+            ly.cout = src.maps; ly.hout = 1; ly.wout = 1;
+            nw = (int64_t)src.maps * c * h * w;
+            nb = src.maps;
+        } else {
+            return fail(CHAOS_EINVAL, "layer %d: unknown kind %d", l, src.kind);
+        }
+        ly.nin = ly.cin * ly.hin * ly.win;
+        ly.nout = ly.cout * ly.hout * ly.wout;
+        if (nw + nb + off > kIntLimit || (int64_t)ly.nout > kIntLimit)
+            return fail(CHAOS_EUNSUPPORTED, "layer %d: sizes beyond 2^30", l);
+        ly.w_off = (int)off;
+        ly.b_off = (int)(off + nw);
+        ly.nw = (int)nw;
+        ly.nb = (int)nb;
+        off += nw + nb;
+        ly.y_off = (int)scr;
+        scr += ly.nout;
+        if (ly.kind == CHAOS_MAXPOOL) {
+            ly.arg_off = (int)scr;  // int32 indices stored in the float scratch
+            scr += ly.nout;
+            ly.d_off = -1;
+        } else {
+            ly.d_off = (int)scr;
+            scr += ly.nout;
+            ly.arg_off = -1;
+        }
+        emax = std::max<int64_t>(emax, std::max(ly.nin, ly.nout));
+        c = ly.cout; h = ly.hout; w = ly.wout;
+    }
+    net.n_layers = n_layers;
+    net.in_size = in_h * in_w;
+    net.n_out = (int)(c * h * w);
+    net.n_params = (int)off;
+    net.e_max = (int)emax;
+    net.e_off0 = (int)scr;
+    net.e_off1 = (int)(scr + emax);
+    scr += 2 * emax;
+    scr = (scr + 63) / 64 * 64;  // keep every worker's area 256-byte aligned
+    if (scr > kIntLimit) return fail(CHAOS_EUNSUPPORTED, "per-worker scratch beyond 2^30 floats");
+    net.scratch_floats = (int)scr;
+    if (net.n_out > 256) return fail(CHAOS_EUNSUPPORTED, "more than 256 outputs");
+    return CHAOS_OK;
+}
+
+int check_net(const chaos_net *net) {
+    if (!net) return fail(CHAOS_EINVAL, "net is NULL");
+    return CHAOS_OK;
+}
+
+int set_device(const chaos_net *net) {
+    HIP_TRY(hipSetDevice(net->device), "hipSetDevice");
+    return CHAOS_OK;
+}
+
+int check_io(const float *x, const int32_t *labels, int64_t n) {
+    if (n < 0) return fail(CHAOS_EINVAL, "n=%lld < 0", (long long)n);
+    if (n > 0 && (!x || !labels)) return fail(CHAOS_EINVAL, "x or labels is NULL");
+    // the claim counter is int32 and may overshoot n by one claim per worker
+    if (n > ((int64_t)1 << 31) - ((int64_t)1 << 24))
+        return fail(CHAOS_EUNSUPPORTED, "n=%lld too large", (long long)n);
+    return CHAOS_OK;
+}
+
+chaos::WorkArgs base_args(chaos_net *net, const float *x, const int32_t *labels, int64_t n) {
+    chaos::WorkArgs a{};
+    a.params = net->params;
+    a.x = x;
+    a.labels = labels;
+    a.n = n;
+    a.scratch = net->scratch;
+    a.counter = net->counter;
+    return a;
+}
+
+} // namespace
+
+extern "C" {
+
+const char *chaos_last_error(void) { return g_last_error.c_str(); }
+
+int chaos_create_net(int32_t in_h, int32_t in_w, const chaos_layer *layers, int32_t n_layers,
+                     const float *init_params_host, int64_t n_params, chaos_net **out) {
+    if (!out) return fail(CHAOS_EINVAL, "out is NULL");
+    *out = nullptr;
+    Net desc;
+    int rc = build_desc(in_h, in_w, layers, n_layers, desc);
+    if (rc) return rc;
+    if (n_params != desc.n_params)
+        return fail(CHAOS_ESHAPE, "n_params=%lld but the architecture has %d weights",
+                    (long long)n_params, desc.n_params);
+    if (!init_params_host) return fail(CHAOS_EINVAL, "init_params_host is NULL");
+
+    chaos_net *net = new (std::nothrow) chaos_net();
+    if (!net) return fail(CHAOS_ENOMEM, "host allocation failed");
+    net->desc = desc;
+    net->n_params = n_params;
+    hipError_t e = hipGetDevice(&net->device);
+    int cus = 0;
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, net->device);
+    if (e != hipSuccess) { delete net; return hip_fail(e, "device query"); }
+    net->block = 256;
+    int per_cu = chaos::worker_blocks_per_cu(net->block);
+    if (per_cu < 1) { delete net; return fail(CHAOS_EDEVICE, "occupancy query failed"); }
+    net->max_workers = per_cu * cus;
+    size_t scratch_bytes = (size_t)net->max_workers * desc.scratch_floats * sizeof(float);
+    e = hipMalloc(&net->params, (size_t)n_params * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(&net->scratch, scratch_bytes);
+    if (e == hipSuccess) e = hipMalloc(&net->counter, 64);
+    if (e == hipSuccess)
+        e = hipMemcpy(net->params, init_params_host, (size_t)n_params * sizeof(float),
+                      hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        chaos_destroy_net(net);
+        return e == hipErrorOutOfMemory ? fail(CHAOS_ENOMEM, "device allocation failed")
+                                        : hip_fail(e, "create");
+    }
+    *out = net;
+    return ok();
+}
+
+int chaos_destroy_net(chaos_net *net) {
+    if (!net) return ok();
+    (void)hipSetDevice(net->device);
+    (void)hipFree(net->params);
+    (void)hipFree(net->scratch);
+    (void)hipFree(net->counter);
+    (void)hipFree(net->grad_part);
+    delete net;
+    return ok();
+}
+
+int64_t chaos_num_params(const chaos_net *net) {
+    if (int rc = check_net(net)) return rc;
+    return net->n_params;
+}
+
+int32_t chaos_num_outputs(const chaos_net *net) {
+    if (int rc = check_net(net)) return rc;
+    return net->desc.n_out;
+}
+
+int32_t chaos_max_workers(const chaos_net *net) {
+    if (int rc = check_net(net)) return rc;
+    return net->max_workers;
+}
+
+int chaos_get_params(const chaos_net *net, float *dst_dev, hipStream_t stream) {
+    if (int rc = check_net(net)) return rc;
+    if (!dst_dev) return fail(CHAOS_EINVAL, "dst_dev is NULL");
+    if (int rc = set_device(net)) return rc;
+    HIP_TRY(hipMemcpyAsync(dst_dev, net->params, (size_t)net->n_params * sizeof(float),
+                           hipMemcpyDeviceToDevice, stream),
+            "get_params");
+    return ok();
+}
+
+int chaos_set_params(chaos_net *net, const float *src_dev, hipStream_t stream) {
+    if (int rc = check_net(net)) return rc;
+    if (!src_dev) return fail(CHAOS_EINVAL, "src_dev is NULL");
+    if (int rc = set_device(net)) return rc;
+    HIP_TRY(hipMemcpyAsync(net->params, src_dev, (size_t)net->n_params * sizeof(float),
+                           hipMemcpyDeviceToDevice, stream),
+            "set_params");
+    return ok();
+}
+
+int chaos_set_claim_counter(chaos_net *net, int32_t *claims_dev) {
+    if (int rc = check_net(net)) return rc;
+    net->claims = claims_dev;
+    return ok();
+}
+
+int chaos_apply_update(chaos_net *net, const float *grad_dev, float lr, hipStream_t stream) {
+    if (int rc = check_net(net)) return rc;
+    if (!grad_dev) return fail(CHAOS_EINVAL, "grad_dev is NULL");
+    if (int rc = set_device(net)) return rc;
+    HIP_TRY(chaos::launch_axpy(net->params, grad_dev, -lr, net->n_params, stream), "apply_update");
+    return ok();
+}
+
+int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_dev, int64_t n,
+                      float lr, int32_t mode, int32_t workers, float *loss_dev,
+                      hipStream_t stream) {
+    if (int rc = check_net(net)) return rc;
+    if (int rc = check_io(x_dev, labels_dev, n)) return rc;
+    if (mode != CHAOS_SEQUENTIAL && mode != CHAOS_HOGWILD_ATOMIC && mode != CHAOS_HOGWILD_RACY)
+        return fail(CHAOS_EINVAL, "unknown mode %d", mode);
+    if (workers < 0 || workers > net->max_workers)
+        return fail(CHAOS_EINVAL, "workers=%d outside [0,%d]", workers, net->max_workers);
+    if (int rc = set_device(net)) return rc;
+    if (n == 0) return ok();
+    int grid = 1;
+    int kmode = chaos::kTrainAtomic;
+    if (mode != CHAOS_SEQUENTIAL) {
+        grid = workers == 0 ? net->max_workers : workers;
+        if (mode == CHAOS_HOGWILD_RACY) kmode = chaos::kTrainRacy;
+    }
+    grid = (int)std::min<int64_t>(grid, n);
+    chaos::WorkArgs a = base_args(net, x_dev, labels_dev, n);
+    a.lr = lr;
+    a.loss = loss_dev;
+    a.claims = net->claims;
+    HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 1, stream), "counter reset");
+    HIP_TRY(chaos::launch_worker(kmode, net->desc, a, grid, net->block, stream), "train launch");
+    return ok();
+}
+
+int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *labels_dev,
+                           int64_t n, float *out_dev, float *loss_dev, float *grad_sum_dev,
+                           float *grad_each_dev, hipStream_t stream) {
+    if (int rc = check_net(net)) return rc;
+    if (int rc = check_io(x_dev, labels_dev, n)) return rc;
+    if (int rc = set_device(net)) return rc;
+    if (n == 0) {
+        if (grad_sum_dev)
+            HIP_TRY(chaos::launch_fill_f32(grad_sum_dev, 0.0f, net->n_params, stream), "zero grad");
+        return ok();
+    }
+    int grid = (int)std::min<int64_t>(net->max_workers, n);
+    if (grad_sum_dev) {
+        // fixed sample -> worker assignment (sample i goes to worker i mod grid,
+        // in increasing i), partial sums per worker, then a fixed-order reduction
+        int want = std::min(grid, 512);
+        if (want > net->fb_workers) {
+            (void)hipFree(net->grad_part);
+            net->grad_part = nullptr;
+            net->fb_workers = 0;
+            hipError_t e = hipMalloc(&net->grad_part, (size_t)want * net->n_params * sizeof(float));
+            if (e != hipSuccess) return fail(CHAOS_ENOMEM, "grad_part allocation failed");
+            net->fb_workers = want;
+        }
+        grid = want;
+    }
+    chaos::WorkArgs a = base_args(net, x_dev, labels_dev, n);
+    a.out = out_dev;
+    a.loss = loss_dev;
+    a.grad_each = grad_each_dev;
+    a.grad_part = grad_sum_dev ? net->grad_part : nullptr;
+    HIP_TRY(chaos::launch_worker(chaos::kForwardBackward, net->desc, a, grid, net->block, stream),
+            "forward_backward launch");
+    if (grad_sum_dev)
+        HIP_TRY(chaos::launch_reduce_partials(net->grad_part, grid, net->n_params, grad_sum_dev,
+                                              stream),
+                "reduce");
+    return ok();
+}
+
+int chaos_evaluate(chaos_net *net, const float *x_dev, const int32_t *labels_dev, int64_t n,
+                   float *out_dev, int32_t *n_wrong_dev, hipStream_t stream) {
+    if (int rc = check_net(net)) return rc;
+    if (int rc = check_io(x_dev, labels_dev, n)) return rc;
+    if (!n_wrong_dev) return fail(CHAOS_EINVAL, "n_wrong_dev is NULL");
+    if (int rc = set_device(net)) return rc;
+    HIP_TRY(chaos::launch_fill_i32(n_wrong_dev, 0, 1, stream), "zero n_wrong");
+    if (n == 0) return ok();
+    int grid = (int)std::min<int64_t>(net->max_workers, n);
+    chaos::WorkArgs a = base_args(net, x_dev, labels_dev, n);
+    a.out = out_dev;
+    a.n_wrong = n_wrong_dev;
+    HIP_TRY(chaos::launch_worker(chaos::kEvaluate, net->desc, a, grid, net->block, stream),
+            "evaluate launch");
+    return ok();
+}
+
+} // extern "C"

@@ -1,0 +1,67 @@
+// Internal descriptors shared by the host API (chaos_api.hip) and the kernels.
+// Plain data only: the net descriptor is passed to kernels by value.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace chaos {
+
+constexpr int kMaxLayers = 16;
+enum LayerKind { kConv = 1, kPool = 2, kFc = 3 };
+
+// One layer after the shape walk.  Offsets index the shared parameter vector
+// (w_off, b_off) or one worker's scratch area (y_off, d_off, arg_off), in
+// floats.
+struct Layer {
+    int kind, k;
+    int cin, hin, win;    // input shape; FC: cin = flattened size, hin = win = 1
+    int cout, hout, wout; // output shape; FC: cout = neurons, hout = wout = 1
+    int nin, nout;        // element counts of input and output
+    int w_off, b_off, nw, nb;
+    int y_off;            // layer output values y
+    int d_off;            // conv/FC: f'(z) of the outputs
+    int arg_off;          // pool: flat input index of each window's maximum
+};
+
+struct Net {
+    int n_layers;
+    int in_size;          // in_h * in_w
+    int n_out;            // size of the last layer's output
+    int n_params;
+    int e_max;            // largest layer input/output size
+    int e_off0, e_off1;   // two error buffers of e_max floats
+    int scratch_floats;   // per-worker scratch size
+    Layer L[kMaxLayers];
+};
+
+enum Mode { kTrainAtomic = 0, kTrainRacy = 1, kForwardBackward = 2, kEvaluate = 3 };
+
+struct WorkArgs {
+    float *params;
+    const float *x;
+    const int32_t *labels;
+    int64_t n;
+    float lr;
+    int32_t *counter;      // dynamic sample claim (training)
+    float *scratch;        // [workers][scratch_floats]
+    float *loss;           // [n] optional
+    float *out;            // [n][n_out] optional
+    float *grad_each;      // [n][n_params] optional
+    float *grad_part;      // [workers][n_params] optional (frozen-weight sums)
+    int32_t *n_wrong;      // [1] evaluation
+    int32_t *claims;       // [n] optional debug claim counter
+};
+
+// Launchers (worker.hip).  Each returns the hipError_t of the launch.
+hipError_t launch_worker(int mode, const Net &net, const WorkArgs &a, int grid, int block,
+                         hipStream_t s);
+hipError_t launch_fill_i32(int32_t *p, int32_t v, int64_t n, hipStream_t s);
+hipError_t launch_fill_f32(float *p, float v, int64_t n, hipStream_t s);
+hipError_t launch_reduce_partials(const float *part, int64_t rows, int64_t cols, float *dst,
+                                  hipStream_t s);
+hipError_t launch_axpy(float *w, const float *g, float alpha, int64_t n, hipStream_t s);
+// Occupancy of the worker kernel: resident blocks per CU for a given block size.
+int worker_blocks_per_cu(int block);
+
+} // namespace chaos
