@@ -19,6 +19,7 @@ struct chaos_net {
     int64_t n_params = 0;
     float *params = nullptr;      // shared weights, canonical layout
     int block = 256;              // threads per worker
+    bool fused = false;           // the fused large-net kernel serves this net
     int max_workers = 0;          // resident workers of the training kernel
     float *scratch = nullptr;     // [max_workers][scratch_floats]
     int32_t *counter = nullptr;   // sample claim counter
@@ -170,6 +171,11 @@ chaos::WorkArgs base_args(chaos_net *net, const float *x, const int32_t *labels,
     return a;
 }
 
+hipError_t launch(chaos_net *net, int mode, const chaos::WorkArgs &a, int grid, hipStream_t s) {
+    if (net->fused) return chaos::launch_fused_large(mode, a, grid, s);
+    return chaos::launch_worker(mode, net->desc, a, grid, net->block, s);
+}
+
 } // namespace
 
 extern "C" {
@@ -197,12 +203,16 @@ int chaos_create_net(int32_t in_h, int32_t in_w, const chaos_layer *layers, int3
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, net->device);
     if (e != hipSuccess) { delete net; return hip_fail(e, "device query"); }
     net->block = 256;
-    int per_cu = chaos::worker_blocks_per_cu(net->block);
+    net->fused = chaos::fused_large_matches(desc);
+    int per_cu = net->fused ? chaos::fused_large_blocks_per_cu()
+                            : chaos::worker_blocks_per_cu(net->block);
     if (per_cu < 1) { delete net; return fail(CHAOS_EDEVICE, "occupancy query failed"); }
     net->max_workers = per_cu * cus;
-    size_t scratch_bytes = (size_t)net->max_workers * desc.scratch_floats * sizeof(float);
+    // the fused kernel keeps every per-sample value in LDS: no scratch
+    size_t scratch_bytes =
+        net->fused ? 0 : (size_t)net->max_workers * desc.scratch_floats * sizeof(float);
     e = hipMalloc(&net->params, (size_t)n_params * sizeof(float));
-    if (e == hipSuccess) e = hipMalloc(&net->scratch, scratch_bytes);
+    if (e == hipSuccess && scratch_bytes) e = hipMalloc(&net->scratch, scratch_bytes);
     if (e == hipSuccess) e = hipMalloc(&net->counter, 64);
     if (e == hipSuccess)
         e = hipMemcpy(net->params, init_params_host, (size_t)n_params * sizeof(float),
@@ -299,7 +309,7 @@ int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_
     a.loss = loss_dev;
     a.claims = net->claims;
     HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 1, stream), "counter reset");
-    HIP_TRY(chaos::launch_worker(kmode, net->desc, a, grid, net->block, stream), "train launch");
+    HIP_TRY(launch(net, kmode, a, grid, stream), "train launch");
     return ok();
 }
 
@@ -334,8 +344,7 @@ int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *la
     a.loss = loss_dev;
     a.grad_each = grad_each_dev;
     a.grad_part = grad_sum_dev ? net->grad_part : nullptr;
-    HIP_TRY(chaos::launch_worker(chaos::kForwardBackward, net->desc, a, grid, net->block, stream),
-            "forward_backward launch");
+    HIP_TRY(launch(net, chaos::kForwardBackward, a, grid, stream), "forward_backward launch");
     if (grad_sum_dev)
         HIP_TRY(chaos::launch_reduce_partials(net->grad_part, grid, net->n_params, grad_sum_dev,
                                               stream),
@@ -355,8 +364,7 @@ int chaos_evaluate(chaos_net *net, const float *x_dev, const int32_t *labels_dev
     chaos::WorkArgs a = base_args(net, x_dev, labels_dev, n);
     a.out = out_dev;
     a.n_wrong = n_wrong_dev;
-    HIP_TRY(chaos::launch_worker(chaos::kEvaluate, net->desc, a, grid, net->block, stream),
-            "evaluate launch");
+    HIP_TRY(launch(net, chaos::kEvaluate, a, grid, stream), "evaluate launch");
     return ok();
 }
 

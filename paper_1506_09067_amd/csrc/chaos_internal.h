@@ -64,4 +64,10 @@ hipError_t launch_axpy(float *w, const float *g, float alpha, int64_t n, hipStre
 // Occupancy of the worker kernel: resident blocks per CU for a given block size.
 int worker_blocks_per_cu(int block);
 
+// Fused MFMA worker for the large net (conv20k4, max2, conv60k3, conv100k6,
+// max2, FC150, FC10 on 29x29 inputs); 256 threads per worker, no scratch.
+bool fused_large_matches(const Net &net);
+hipError_t launch_fused_large(int mode, const WorkArgs &a, int grid, hipStream_t s);
+int fused_large_blocks_per_cu();
+
 } // namespace chaos
