@@ -344,6 +344,9 @@ int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *la
     a.loss = loss_dev;
     a.grad_each = grad_each_dev;
     a.grad_part = grad_sum_dev ? net->grad_part : nullptr;
+    if (grad_sum_dev)
+        HIP_TRY(chaos::launch_fill_f32(net->grad_part, 0.0f, (int64_t)grid * net->n_params, stream),
+                "zero partial sums");
     HIP_TRY(launch(net, chaos::kForwardBackward, a, grid, stream), "forward_backward launch");
     if (grad_sum_dev)
         HIP_TRY(chaos::launch_reduce_partials(net->grad_part, grid, net->n_params, grad_sum_dev,

@@ -27,13 +27,19 @@ __device__ __forceinline__ float wave_sum(float v) {
     return v;
 }
 
+// Where a layer's weight gradient g goes (per element, once per sample):
+//   training   W[off] += -lr * g, an atomic fp32 add or a racy load/add/store
+//   frozen     each[off] = g (per-sample row) and/or part[off] += g, an atomic
+//              add into this worker's own zero-initialised row.  A worker's
+//              samples are separated by barriers that wait for its memory
+//              operations, so the adds into a row happen in sample order and
+//              the partial sums are reproducible bit for bit.
 struct Push {
     int mode;
     float *params;
     float neg_lr;
     float *each;  // this sample's gradient row or null
     float *part;  // this worker's partial-sum row or null
-    bool first;   // first sample of this worker: partial row is overwritten
 
     __device__ __forceinline__ void operator()(int off, float g) const {
         if (mode == kTrainAtomic) {
@@ -47,7 +53,8 @@ struct Push {
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         } else {
             if (each) each[off] = g;
-            if (part) part[off] = first ? g : part[off] + g;
+            if (part)
+                __hip_atomic_fetch_add(part + off, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 };

@@ -70,16 +70,19 @@ struct alignas(16) Smem {
             float d3[C3 * M3P];          // conv3 output deltas, rows (P, w)
         };
         float red3[2 * 21 * 256];        // conv3 split-K partial sums (forward only)
+        float w2s[KC2 * 65];             // conv2 weights staged as [k][o] (forward only)
     };
     float p3[NF1];                       // pool2 output (FC1 input)
     float e3[NF1];                       // dE/d(pool2 output)
     float h[F1 + 10], dh[F1 + 10];
     float o[16], dout[16];
+    alignas(16) int koff3[KC3];          // im2col offset into y2 of k = (c,u,v), conv3
+    alignas(16) int koff2[KC2 + 4];      // im2col offset into p1 of k = (c,u,v), conv2
     unsigned char am1[C1 * NP1 + 12];    // pool1 argmax (window element 0..3)
     unsigned char am3[NF1 + 4];          // pool2 argmax
-    float red[NW];
     int64_t idx;
 };
+static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
 
 // scaled tanh without its derivative (forward epilogues)
 __device__ __forceinline__ float act_y(float z) {
@@ -115,13 +118,28 @@ __device__ __forceinline__ int window_pos(int P, int w, int pw, int wd) {
 template <int MODE>
 __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
     __shared__ Smem sm;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int lr = lane & 15, lg = lane >> 4;
+    const int tid = threadIdx.x;
     const float *W = a.params;
     constexpr bool kTrain = (MODE == kTrainAtomic || MODE == kTrainRacy);
-    int64_t step = 0;
 
-    for (;; ++step) {
+    // sample-invariant im2col offset tables
+    for (int k = tid; k < KC3; k += NT) {
+        int c = k / 36, uv = k - 36 * c, u = uv / 6, v = uv - 6 * u;
+        sm.koff3[k] = c * NY2 + u * H2 + v;
+    }
+    for (int k = tid; k < KC2 + 4; k += NT) {
+        int c = k / 9, uv = k - 9 * c, u = uv / 3, v = uv - 3 * u;
+        sm.koff2[k] = (k < KC2) ? c * NP1 + u * Q1 + v : 0;
+    }
+
+    for (int64_t step = 0;; ++step) {
+        // The thread index is made opaque to the optimizer at the top of each
+        // sample: index arithmetic of every phase then stays inside its phase
+        // instead of being hoisted out of this loop and kept live throughout.
+        int tid_l = threadIdx.x;
+        asm volatile("" : "+v"(tid_l));
+        const int lane = tid_l & 63, lr = lane & 15, lg = lane >> 4;
+        const int wave = __builtin_amdgcn_readfirstlane(tid_l >> 6);
         // ---- claim a sample (Section III-A.1) ----
         if (tid == 0) sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1)
                                       : (int64_t)blockIdx.x + step * gridDim.x;
@@ -135,6 +153,15 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         }
         const int label = a.labels[idx];
         for (int i = tid; i < NX; i += NT) sm.x[i] = a.x[idx * NX + i];
+        // conv2 weights staged in LDS as [k][o] (o padded to 65 to spread banks)
+        for (int t = tid; t < C2 * KC2; t += NT) {
+            int o = t / KC2, k = t - o * KC2;
+            sm.w2s[k * 65 + o] = W[OW2 + t];
+        }
+        for (int t = tid; t < KC2 * 5; t += NT) {
+            int k = t / 5, o = C2 + (t - 5 * k);
+            sm.w2s[k * 65 + o] = 0.0f;
+        }
         __syncthreads();
 
         // ================= forward propagation =================
@@ -179,7 +206,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         }
         __syncthreads();
 
-        // conv2: rows p < 121 (8 tiles), cols o < 60 (4 tiles), K = 180
+        // conv2: rows p < 121 (8 tiles), cols o < 60 (4 tiles), K = 180; all operands in LDS
         {
             f4 acc[2][4];
 #pragma unroll
@@ -195,18 +222,15 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 int py = p / H2, px = p - py * H2;
                 base[t] = valid[t] ? py * Q1 + px : 0;
             }
+#pragma unroll 3
             for (int ks = 0; ks < KC2 / 4; ++ks) {
                 int k = 4 * ks + lg;
-                int c = k / 9, uv = k - 9 * c, u = uv / 3, v = uv - 3 * u;
-                int off = c * NP1 + u * Q1 + v;
+                int off = sm.koff2[k];
                 float av[2], bv[4];
 #pragma unroll
                 for (int t = 0; t < 2; ++t) av[t] = valid[t] ? sm.p1[base[t] + off] : 0.0f;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    int o = 16 * j + lr;
-                    bv[j] = (o < C2) ? W[OW2 + o * KC2 + k] : 0.0f;
-                }
+                for (int j = 0; j < 4; ++j) bv[j] = sm.w2s[k * 65 + 16 * j + lr];
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -229,7 +253,10 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         __syncthreads();
 
         // conv3 + pool2: rows m = 4P + w (36 -> 3 tiles), cols o < 100 (7 tiles),
-        // K = 2160 split across the 4 wavefronts (15 input maps each)
+        // K = 2160 in 135 super-steps of 16, split 34/34/34/33 over the wavefronts.
+        // Within a super-step lane group g holds k = 16S + 4g + s at sub-step s,
+        // so each lane reads its four weights of a super-step with one 16-byte
+        // load; the next super-step's weights are loaded while this one computes.
         {
             f4 acc[3][7];
 #pragma unroll
@@ -244,26 +271,41 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 valid[i] = m < M3;
                 base[i] = valid[i] ? window_pos(m >> 2, m & 3, 3, H2) : 0;
             }
-            const int ks0 = wave * (KC3 / 4 / NW), ks1 = ks0 + KC3 / 4 / NW;
-            for (int ks = ks0; ks < ks1; ++ks) {
-                int k = 4 * ks + lg;
-                int c = k / 36, uv = k - 36 * c, u = uv / 6, v = uv - 6 * u;
-                int off = c * NY2 + u * H2 + v;
-                float av[3], bv[7];
-#pragma unroll
-                for (int i = 0; i < 3; ++i) av[i] = valid[i] ? sm.y2[base[i] + off] : 0.0f;
+            const int S0 = wave * 34, S1 = (S0 + 34 < 135) ? S0 + 34 : 135;
+            f4 bA[7], bB[7];
+            auto load_b = [&](f4 (&b)[7], int S) {
 #pragma unroll
                 for (int j = 0; j < 7; ++j) {
                     int o = 16 * j + lr;
-                    bv[j] = (o < C3) ? W[OW3 + o * KC3 + k] : 0.0f;
+                    b[j] = (o < C3) ? *(const f4 *)(W + OW3 + o * KC3 + 16 * S + 4 * lg)
+                                    : f4{0.f, 0.f, 0.f, 0.f};
                 }
+            };
+            auto compute = [&](const f4 (&b)[7], int S) {
+                const int4 ko = *(const int4 *)(sm.koff3 + 16 * S + 4 * lg);
+                const int offs[4] = {ko.x, ko.y, ko.z, ko.w};
 #pragma unroll
-                for (int i = 0; i < 3; ++i)
+                for (int s = 0; s < 4; ++s) {
+                    float av[3];
 #pragma unroll
-                    for (int j = 0; j < 7; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
+                    for (int i = 0; i < 3; ++i) av[i] = valid[i] ? sm.y2[base[i] + offs[s]] : 0.0f;
+#pragma unroll
+                    for (int i = 0; i < 3; ++i)
+#pragma unroll
+                        for (int j = 0; j < 7; ++j) acc[i][j] = mfma(av[i], b[j][s], acc[i][j]);
+                }
+            };
+            load_b(bA, S0);
+            for (int S = S0; S < S1; S += 2) {
+                if (S + 1 < S1) load_b(bB, S + 1);
+                compute(bA, S);
+                if (S + 1 < S1) {
+                    if (S + 2 < S1) load_b(bA, S + 2);
+                    compute(bB, S + 1);
+                }
             }
-            // fixed-order reduction of the four partial sums through LDS:
-            // (w0 + w2) + (w1 + w3)
+            // fixed-order reduction (w0 + w2) + (w1 + w3) through LDS; the
+            // epilogue of col tiles 0..3 runs on wavefront 0, of 4..6 on 1
             float *buf = sm.red3;  // 2 x 21 tiles x 64 lanes x 4 floats
             if (wave >= 2) {
                 float *dst = buf + (wave - 2) * (21 * 256);
@@ -283,17 +325,20 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                         acc[i][j] += *(const f4 *)(src + ((i * 7 + j) * 64 + lane) * 4);
             }
             __syncthreads();
-            if (wave == 1) {
+            if (wave < 2) {
+                // wavefront 0 hands over tiles 4..6, wavefront 1 tiles 0..3
 #pragma unroll
                 for (int i = 0; i < 3; ++i)
 #pragma unroll
                     for (int j = 0; j < 7; ++j)
-                        *(f4 *)(buf + ((i * 7 + j) * 64 + lane) * 4) = acc[i][j];
+                        if ((j >= 4) == (wave == 0))
+                            *(f4 *)(buf + ((i * 7 + j) * 64 + lane) * 4) = acc[i][j];
             }
             __syncthreads();
-            if (wave == 0) {
+            if (wave < 2) {
 #pragma unroll
                 for (int j = 0; j < 7; ++j) {
+                    if ((j >= 4) != (wave == 1)) continue;
                     int o = 16 * j + lr;
                     if (o >= C3) continue;
                     float bias = W[OB3 + o];
@@ -314,20 +359,41 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         }
         __syncthreads();
 
-        // FC1: one wavefront per neuron, lanes across the 900 inputs
-        for (int j = wave; j < F1; j += NW) {
-            const float *wj = W + OF1 + j * NF1;
-            float s = 0.0f;
-            for (int i = lane; i < NF1; i += 64) s = fmaf(wj[i], sm.p3[i], s);
-            s = wave_sum(s);
-            if (lane == 0) sm.h[j] = act_y(s + W[OBF1 + j]);
+        // FC1: four neurons per wavefront at a time, lanes across the 900
+        // inputs; all 60 weight loads of a round are issued before the sums
+        for (int j0 = 4 * wave; j0 < F1; j0 += 4 * NW) {
+            float wv[4][15];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int it = 0; it < 15; ++it) {
+                    int j = j0 + q, i = lane + 64 * it;
+                    wv[q][it] = (j < F1 && i < NF1) ? W[OF1 + j * NF1 + i] : 0.0f;
+                }
+            float s[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int it = 0; it < 15; ++it) {
+                int i = lane + 64 * it;
+                float xi = (i < NF1) ? sm.p3[i] : 0.0f;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) s[q] = fmaf(wv[q][it], xi, s[q]);
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                float t = wave_sum(s[q]);
+                if (lane == 0 && j0 + q < F1) sm.h[j0 + q] = act_y(t + W[OBF1 + j0 + q]);
+            }
         }
         __syncthreads();
         // FC2 (output layer)
         for (int j = wave; j < F2; j += NW) {
             const float *wj = W + OF2 + j * F1;
             float s = 0.0f;
-            for (int i = lane; i < F1; i += 64) s = fmaf(wj[i], sm.h[i], s);
+#pragma unroll
+            for (int it = 0; it < 3; ++it) {
+                int i = lane + 64 * it;
+                if (i < F1) s = fmaf(wj[i], sm.h[i], s);
+            }
             s = wave_sum(s);
             if (lane == 0) sm.o[j] = act_y(s + W[OBF2 + j]);
         }
@@ -352,7 +418,6 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         push.neg_lr = -a.lr;
         push.each = a.grad_each ? a.grad_each + idx * (int64_t)NPARAM : nullptr;
         push.part = a.grad_part ? a.grad_part + (int64_t)blockIdx.x * NPARAM : nullptr;
-        push.first = (step == 0);
 
         // output layer: E = 1/2 sum (y - t)^2, delta = (y - t) f'(z)
         if (tid < 64) {
@@ -368,23 +433,46 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         }
         __syncthreads();
         // FC2 backward data (pre-update weights)
-        for (int i = tid; i < F1; i += NT) {
+        if (tid < F1) {
+            float wv[F2];
+#pragma unroll
+            for (int j = 0; j < F2; ++j) wv[j] = W[OF2 + j * F1 + tid];
             float s = 0.0f;
 #pragma unroll
-            for (int j = 0; j < F2; ++j) s = fmaf(W[OF2 + j * F1 + i], sm.dout[j], s);
-            sm.dh[i] = s * dact_from_y(sm.h[i]);
+            for (int j = 0; j < F2; ++j) s = fmaf(wv[j], sm.dout[j], s);
+            sm.dh[tid] = s * dact_from_y(sm.h[tid]);
         }
         __syncthreads();
-        // FC2 push; FC1 backward data
+        // FC2 push; FC1 backward data (pre-update weights): thread per input,
+        // weights loaded 10 neurons at a time for 4 inputs per thread
         for (int t = tid; t < F2 * F1; t += NT) {
             int j = t / F1, i = t - j * F1;
             push(OF2 + t, sm.dout[j] * sm.h[i]);
         }
         if (tid < F2) push(OBF2 + tid, sm.dout[tid]);
-        for (int i = tid; i < NF1; i += NT) {
-            float s = 0.0f;
-            for (int j = 0; j < F1; ++j) s = fmaf(W[OF1 + j * NF1 + i], sm.dh[j], s);
-            sm.e3[i] = s;
+        {
+            float s[4] = {0.f, 0.f, 0.f, 0.f};
+            for (int j0 = 0; j0 < F1; j0 += 10) {
+                float wv[4][10];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int jj = 0; jj < 10; ++jj) {
+                        int i = tid + NT * q;
+                        wv[q][jj] = (i < NF1) ? W[OF1 + (j0 + jj) * NF1 + i] : 0.0f;
+                    }
+#pragma unroll
+                for (int jj = 0; jj < 10; ++jj) {
+                    float d = sm.dh[j0 + jj];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) s[q] = fmaf(wv[q][jj], d, s[q]);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                int i = tid + NT * q;
+                if (i < NF1) sm.e3[i] = s[q];
+            }
         }
         __syncthreads();
         // FC1 push; pool2 backward -> conv3 output deltas d3[o][4P + w]; clear s2
@@ -406,9 +494,14 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         __syncthreads();
 
         // conv3 backward data: C[k][m] = sum_o W3[o][k] d3[o][m], k = (c,u,v);
-        // col2im into s2[c][pos(m) + (u,v)].  Wavefront w owns input maps
-        // c in blocks of 4 (144 rows = 9 tiles), so no two wavefronts touch
-        // the same s2 entries.
+        // col2im into s2[c][pos(m) + (u,v)].  Wavefront w owns input maps in
+        // blocks of 4 (144 rows = 9 tiles), so no two wavefronts touch the
+        // same s2 entries.  Row q of tile i holds input map c0 + q/4 at kernel
+        // offset uv = 4i + q%4: in the accumulator the four lane groups then
+        // hold four different maps at one (u,v), so no scatter instruction
+        // has two lanes on one address.  Different instructions do meet
+        // (lanes are threads: those adds are LDS atomics).  The next output
+        // map's weights are loaded while the current one computes.
         for (int blk = wave; blk < C2 / 4; blk += NW) {
             f4 acc[9][3];
 #pragma unroll
@@ -416,31 +509,45 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                 for (int j = 0; j < 3; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
             const int k0 = blk * 144;
-            for (int ks = 0; ks < C3 / 4; ++ks) {
-                int o = 4 * ks + lg;
-                float av[9], bv[3];
+            const int arow = k0 + (lr >> 2) * 36 + (lr & 3);
+            float aA[9], aB[9];
+            auto load_a = [&](float (&av)[9], int ks) {
+                const float *w3 = W + OW3 + (4 * ks + lg) * KC3 + arow;
 #pragma unroll
-                for (int i = 0; i < 9; ++i) av[i] = W[OW3 + o * KC3 + k0 + 16 * i + lr];
+                for (int i = 0; i < 9; ++i) av[i] = w3[4 * i];
+            };
+            auto compute = [&](const float (&av)[9], int ks) {
+                const float *dd = sm.d3 + (4 * ks + lg) * M3P + lr;
+                float bv[3];
 #pragma unroll
-                for (int j = 0; j < 3; ++j) bv[j] = sm.d3[o * M3P + 16 * j + lr];
+                for (int j = 0; j < 3; ++j) bv[j] = dd[16 * j];
 #pragma unroll
                 for (int i = 0; i < 9; ++i)
 #pragma unroll
                     for (int j = 0; j < 3; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
+            };
+            load_a(aA, 0);
+            for (int ks = 0; ks < C3 / 4; ks += 2) {
+                if (ks + 1 < C3 / 4) load_a(aB, ks + 1);
+                compute(aA, ks);
+                if (ks + 1 < C3 / 4) {
+                    if (ks + 2 < C3 / 4) load_a(aA, ks + 2);
+                    compute(aB, ks + 1);
+                }
             }
+            float *dst = sm.s2 + (4 * blk + lg) * NY2;
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
                 int m = 16 * j + lr;
                 if (m >= M3) continue;
-                int pos = window_pos(m >> 2, m & 3, 3, H2);
+                float *dm = dst + window_pos(m >> 2, m & 3, 3, H2);
 #pragma unroll
                 for (int i = 0; i < 9; ++i)
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        int k = k0 + 16 * i + 4 * lg + r;
-                        int c = k / 36, uv = k - 36 * c, u = uv / 6, v = uv - 6 * u;
-                        __hip_atomic_fetch_add(&sm.s2[c * NY2 + pos + u * H2 + v], acc[i][j][r],
-                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                        const int uv = 4 * i + r, u = uv / 6, v = uv - 6 * u;
+                        __hip_atomic_fetch_add(dm + u * H2 + v, acc[i][j][r], __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_WORKGROUP);
                     }
             }
         }
@@ -456,22 +563,16 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     int o = 16 * i + lr;
                     ad[i][s] = (o < C3) ? sm.d3[o * M3P + 4 * s + lg] : 0.0f;
                 }
-            int pos[9];
-#pragma unroll
-            for (int s = 0; s < 9; ++s) {
-                int m = 4 * s + lg;
-                pos[s] = window_pos(m >> 2, m & 3, 3, H2);
-            }
             for (int jt = wave; jt < KC3 / 16; jt += NW) {
                 int k = 16 * jt + lr;
-                int c = k / 36, uv = k - 36 * c, u = uv / 6, v = uv - 6 * u;
-                const float *ycol = sm.y2 + c * NY2 + u * H2 + v;
+                const float *ycol = sm.y2 + sm.koff3[k];
                 f4 acc[7];
 #pragma unroll
                 for (int i = 0; i < 7; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int s = 0; s < 9; ++s) {
-                    float bv = ycol[pos[s]];
+                    int m = 4 * s + lg;
+                    float bv = ycol[window_pos(m >> 2, m & 3, 3, H2)];
 #pragma unroll
                     for (int i = 0; i < 7; ++i) acc[i] = mfma(ad[i][s], bv, acc[i]);
                 }
@@ -498,56 +599,83 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         }
         __syncthreads();
 
-        // conv2 backward data: C[k][p] = sum_o W2[o][k] d2[o][p], k = (c,u,v) < 180;
-        // col2im into e1[c][p + (u,v)] (13x13 maps), wavefront by wavefront
+        // conv2 backward data: C[k][p] = sum_o W2[o][k] d2[o][p], k = (c,u,v);
+        // col2im into e1[c][p + (u,v)] (13x13 maps).  Wavefront w owns input
+        // maps 5w..5w+4, so col2im needs no ordering between wavefronts.
+        // Tiles 0..2 hold maps 5w + q/4 at uv = 4i + q%4 (no two lanes of one
+        // scatter instruction on one address, as for conv3); tile 3 holds map
+        // 5w + 4 at uv = q.
         {
-            f4 acc[3][8];
+            f4 acc[4][8];
 #pragma unroll
-            for (int i = 0; i < 3; ++i)
+            for (int i = 0; i < 4; ++i)
 #pragma unroll
                 for (int j = 0; j < 8; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
-            for (int ks = 0; ks < C2 / 4; ++ks) {
-                int o = 4 * ks + lg;
-                float av[3], bv[8];
+            const int c0 = 5 * wave;
+            // row of this lane in each tile: k index (or -1 when padding)
+            int krow[4];
 #pragma unroll
-                for (int i = 0; i < 3; ++i) {
-                    int k = 16 * (3 * wave + i) + lr;
-                    av[i] = (k < KC2) ? W[OW2 + o * KC2 + k] : 0.0f;
-                }
+            for (int i = 0; i < 3; ++i) {
+                int uv = 4 * i + (lr & 3);
+                krow[i] = (uv < 9) ? (c0 + (lr >> 2)) * 9 + uv : -1;
+            }
+            krow[3] = (lr < 9) ? (c0 + 4) * 9 + lr : -1;
+            float aA[4], aB[4];
+            auto load_a = [&](float (&av)[4], int ks) {
+                const float *w2 = W + OW2 + (4 * ks + lg) * KC2;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) av[i] = (krow[i] >= 0) ? w2[krow[i]] : 0.0f;
+            };
+            auto compute = [&](const float (&av)[4], int ks) {
+                const float *dd = sm.y2 + (4 * ks + lg) * NY2;
+                float bv[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     int p = 16 * j + lr;
-                    bv[j] = (p < NY2) ? sm.y2[o * NY2 + p] : 0.0f;
+                    bv[j] = (p < NY2) ? dd[p] : 0.0f;
                 }
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
+            };
+            load_a(aA, 0);
+            for (int ks = 0; ks < C2 / 4; ks += 2) {
+                if (ks + 1 < C2 / 4) load_a(aB, ks + 1);
+                compute(aA, ks);
+                if (ks + 1 < C2 / 4) {
+                    if (ks + 2 < C2 / 4) load_a(aA, ks + 2);
+                    compute(aB, ks + 1);
+                }
+            }
+            float *e1 = sm.s2;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                int p = 16 * j + lr;
+                if (p >= NY2) continue;
+                int py = p / H2, px = p - py * H2;
+                float *dp = e1 + py * Q1 + px;
+                float *dm = dp + (c0 + lg) * NP1;
 #pragma unroll
                 for (int i = 0; i < 3; ++i)
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
-            }
-            float *e1 = sm.s2;
-            for (int turn = 0; turn < NW; ++turn) {
-                if (wave == turn) {
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        int p = 16 * j + lr;
-                        if (p >= NY2) continue;
-                        int py = p / H2, px = p - py * H2;
-#pragma unroll
-                        for (int i = 0; i < 3; ++i)
-#pragma unroll
-                            for (int r = 0; r < 4; ++r) {
-                                int k = 16 * (3 * wave + i) + 4 * lg + r;
-                                if (k >= KC2) continue;
-                                int c = k / 9, uv = k - 9 * c, u = uv / 3, v = uv - 3 * u;
-                                __hip_atomic_fetch_add(&e1[c * NP1 + (py + u) * Q1 + px + v],
-                                                       acc[i][j][r], __ATOMIC_RELAXED,
-                                                       __HIP_MEMORY_SCOPE_WORKGROUP);
-                            }
+                    for (int r = 0; r < 4; ++r) {
+                        const int uv = 4 * i + r, u = uv / 3, v = uv - 3 * u;
+                        if (uv < 9)
+                            __hip_atomic_fetch_add(dm + u * Q1 + v, acc[i][j][r], __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_WORKGROUP);
                     }
+                float *d4 = dp + (c0 + 4) * NP1;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    int uv = 4 * lg + r, u = uv / 3, v = uv - 3 * u;
+                    if (uv < 9)
+                        __hip_atomic_fetch_add(d4 + u * Q1 + v, acc[3][j][r], __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_WORKGROUP);
                 }
-                __syncthreads();
             }
         }
+        __syncthreads();
 
         // conv2 weight gradient: G[o][k] = sum_p d2[o][p] p1col[p][k], pushed;
         // pool1 backward: e1 <- e1 * f'(pool1 value) (delta at each window's max)
@@ -563,8 +691,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             for (int j = 0; j < 3; ++j) {
                 int k = 16 * (3 * wave + j) + lr;
                 kval[j] = k < KC2;
-                int c = k / 9, uv = k - 9 * c, u = uv / 3, v = uv - 3 * u;
-                boff[j] = kval[j] ? c * NP1 + u * Q1 + v : 0;
+                boff[j] = kval[j] ? sm.koff2[k] : 0;
             }
             for (int ks = 0; ks < 31; ++ks) {
                 int p = 4 * ks + lg;
@@ -612,8 +739,13 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 int o = t >> 4, u = (t >> 2) & 3, v = t & 3;
                 const float *d1 = sm.s2 + o * NP1;
                 const unsigned char *am = sm.am1 + o * NP1;
-                for (int P = 0; P < NP1; ++P)
-                    g = fmaf(d1[P], sm.x[window_pos(P, am[P], Q1, IN) + u * IN + v], g);
+                const float *xs = sm.x + u * IN + v;
+                for (int py = 0; py < Q1; ++py)
+#pragma unroll
+                    for (int px = 0; px < Q1; ++px) {
+                        int P = py * Q1 + px, w = am[P];
+                        g = fmaf(d1[P], xs[(2 * py + (w >> 1)) * IN + 2 * px + (w & 1)], g);
+                    }
                 push(OW1 + t, g);
             } else {
                 int o = t - C1 * 16;

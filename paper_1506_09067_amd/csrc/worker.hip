@@ -234,7 +234,6 @@ __global__ void __launch_bounds__(256) worker_kernel(Net net, WorkArgs a) {
         push.neg_lr = -a.lr;
         push.each = a.grad_each ? a.grad_each + idx * (int64_t)net.n_params : nullptr;
         push.part = a.grad_part ? a.grad_part + (int64_t)blockIdx.x * net.n_params : nullptr;
-        push.first = (step == 0);
         float *e = e0, *ep = e1;
         for (int l = net.n_layers - 1; l >= 0; --l) {
             const Layer &ly = net.L[l];
