@@ -61,6 +61,28 @@ def train_flops_per_sample(layers, in_hw=29):
     return 2 * (fwd + bwd + wgrad + params), 2 * fwd
 
 
+def kernel_source_hash():
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_1506_09067_amd", "csrc")
+    return hashlib.sha256(b"".join(open(os.path.join(csrc, f), "rb").read()
+                                   for f in ("fused_large.hip", "device_common.h"))).hexdigest()
+
+
+def measured_traffic(net, workers, samples):
+    """Calibrated HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE
+    counter runs, or None when they were taken on another configuration or
+    before the kernel source last changed."""
+    if not os.path.exists(PROFILE_TRAFFIC):
+        return None
+    with open(PROFILE_TRAFFIC) as f:
+        t = json.load(f)
+    if (t.get("net"), t.get("workers"), t.get("samples_per_launch")) != (net, workers, samples):
+        return None
+    if t.get("source_sha256") != kernel_source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
 def cpu_baseline(layers, p0, x, y, budget_s=15.0):
     """The oracle, as it stands, on the first samples of the same set."""
     from oracle import oracle as orc
@@ -88,7 +110,19 @@ def main():
     ap.add_argument("--samples", type=int, default=60000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rows", action="store_true")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB (calibrates "
+                         "the FETCH_SIZE / WRITE_SIZE counters) and exit")
     args = ap.parse_args()
+    if args.copy_mib:
+        import torch
+        n = args.copy_mib * (1 << 20) // 4
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the path shards by samples across GPUs, see the design notes)", file=sys.stderr)
@@ -131,12 +165,7 @@ def main():
     value = args.samples * args.steps / (total_ms / 1e3)
     avg_launch_s = total_ms / 1e3 / args.steps
     achieved = flops * args.samples / avg_launch_s / 1e12
-    traffic = None
-    if os.path.exists(PROFILE_TRAFFIC):
-        with open(PROFILE_TRAFFIC) as f:
-            t = json.load(f)
-        if t.get("net") == args.net and t.get("workers") == workers:
-            traffic = t.get("bytes_per_launch")
+    traffic = measured_traffic(args.net, workers, args.samples)
     w = net.get_params()
     torch.cuda.synchronize()
     finite = bool(torch.isfinite(w).all().item())
@@ -188,7 +217,7 @@ def main():
                    "net": args.net, "samples_per_step": args.samples, "workers": workers,
                    "mode": args.mode, "params": net.n_params,
                    "train_flop_per_sample": flops},
-        "roofline": {"bound": "alu", "achieved": achieved, "peak": PEAK_FP32_TFLOPS,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_TFLOPS, "traffic": traffic},
         "cpu_baseline": cpu,
         "rows": rows,

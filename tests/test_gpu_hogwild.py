@@ -1,0 +1,74 @@
+"""Hogwild acceptance on MI355X: training with many concurrent lock-free
+workers ends within 1% of sequential per-sample SGD on the same seeded data.
+
+Hogwild results are not deterministic (Section IV-B attributes the spread in
+Table II to the non-deterministic weight updates), so they are compared with
+the sequential run statistically: final test-set loss within 1% (relative)
+and accuracy within 1 percentage point.  Sequential SGD itself is checked
+against the oracle in test_gpu_parity.py.
+"""
+import numpy as np
+import pytest
+
+from paper_1506_09067_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_1506_09067_amd import chaos
+    chaos.lib()
+    return torch, chaos
+
+
+def _train_and_test(torch, chaos, name, x, y, xt, yt, epochs, lr, decay, mode, workers):
+    layers = wl.NETS[name]
+    net = chaos.Net(layers, wl.init_params(layers))
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    for ep in range(epochs):
+        net.train_epoch(xd, yd, lr * decay ** ep, mode=mode, workers=workers)
+    xtd, ytd = torch.from_numpy(xt).cuda(), torch.from_numpy(yt).cuda()
+    loss = torch.empty(len(yt), device="cuda")
+    net.forward_backward(xtd, ytd, loss=loss)
+    wrong = net.evaluate(xtd, ytd)
+    w = net.get_params()
+    torch.cuda.synchronize()
+    assert torch.isfinite(w).all()
+    return float(loss.double().mean()), 1.0 - int(wrong.item()) / len(yt), net.max_workers
+
+
+# (net, training samples, epochs, lr, Hogwild workers; 0 = every resident worker).
+# With every resident worker (256) at lr 1e-3 the large net's first wave of
+# gradients, all computed at the initial weights, lands at once: about half of
+# the runs show a transient loss spike near sample 300 and one run in ~13 did
+# not recover.  The acceptance runs therefore use 64 workers at lr 1e-3 and
+# every worker at lr 5e-4 (no spike in 16 runs each).
+CASES = [
+    ("small", 20000, 3, 1e-3, 256),
+    ("large", 20000, 1, 1e-3, 64),
+    ("large", 20000, 1, 5e-4, 0),
+]
+
+
+@pytest.mark.parametrize("name,n,epochs,lr,workers", CASES)
+def test_hogwild_matches_sequential_sgd(env, name, n, epochs, lr, workers):
+    torch, chaos = env
+    x, y = wl.train_set(n)
+    xt, yt = wl.test_set(5000)
+    decay = 0.9
+    seq = _train_and_test(torch, chaos, name, x, y, xt, yt, epochs, lr, decay, chaos.SEQUENTIAL, 0)
+    hog = _train_and_test(torch, chaos, name, x, y, xt, yt, epochs, lr, decay,
+                          chaos.HOGWILD_ATOMIC, workers)
+    # the sequential run learned something, so the comparison is not vacuous
+    init = _train_and_test(torch, chaos, name, x[:0], y[:0], xt, yt, 1, lr, decay,
+                           chaos.SEQUENTIAL, 0)
+    assert seq[0] < init[0]
+    msg = (f"{name}: sequential loss {seq[0]:.5f} acc {seq[1]:.4f}; Hogwild with "
+           f"{workers or hog[2]} workers loss {hog[0]:.5f} acc {hog[1]:.4f}; "
+           f"untrained loss {init[0]:.5f}")
+    assert abs(hog[0] - seq[0]) <= 0.01 * seq[0], msg
+    assert abs(hog[1] - seq[1]) <= 0.01, msg
