@@ -70,4 +70,10 @@ bool fused_large_matches(const Net &net);
 hipError_t launch_fused_large(int mode, const WorkArgs &a, int grid, hipStream_t s);
 int fused_large_blocks_per_cu();
 
+// Fused MFMA workers for the Table I small (variant 1) and medium (variant 2)
+// nets: conv C1@4x4, max2, conv C2@5x5, max3, FC F1, FC10 on 29x29 inputs.
+int fused_cpcp_variant(const Net &net);  // 0 when the net is neither
+hipError_t launch_fused_cpcp(int variant, int mode, const WorkArgs &a, int grid, hipStream_t s);
+int fused_cpcp_blocks_per_cu(int variant);
+
 } // namespace chaos

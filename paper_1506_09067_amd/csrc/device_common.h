@@ -59,4 +59,41 @@ struct Push {
     }
 };
 
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f4 mfma(float a, float b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// scaled tanh without its derivative (forward epilogues)
+__device__ __forceinline__ float act_y(float z) {
+    float y, d;
+    activation(z, y, d);
+    return y;
+}
+
+// f'(z) from y = f(z): A B (1 - (y/A)^2) = (B/A)(A^2 - y^2)
+__device__ __forceinline__ float dact_from_y(float y) {
+    return (kActB / kActA) * (kActA * kActA - y * y);
+}
+
+// Max over a 2x2 window held in one lane's accumulator (window elements in
+// row-major order); the first maximum wins.
+__device__ __forceinline__ void pool4(f4 acc, float bias, float &ymax, int &arg) {
+    ymax = act_y(acc[0] + bias);
+    arg = 0;
+#pragma unroll
+    for (int r = 1; r < 4; ++r) {
+        float y = act_y(acc[r] + bias);
+        if (y > ymax) { ymax = y; arg = r; }
+    }
+}
+
+// position (row-major index into a map of width `wd`) of element w of the
+// 2x2 window of pooled position P on a pooled grid of width `pw`
+__device__ __forceinline__ int window_pos(int P, int w, int pw, int wd) {
+    int py = P / pw, px = P - py * pw;
+    return (2 * py + (w >> 1)) * wd + 2 * px + (w & 1);
+}
+
 } // namespace chaos

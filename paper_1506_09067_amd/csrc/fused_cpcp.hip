@@ -1,0 +1,502 @@
+// Fused per-sample CHAOS worker for the Table I small and medium nets:
+//   1x29x29 -> conv C1@4x4 -> max 2 -> conv C2@5x5 -> max 3 -> FC F1 -> FC 10
+//   small: C1 = 5, C2 = 10, F1 = 50;  medium: C1 = 20, C2 = 40, F1 = 150.
+//
+// Same organisation as the large-net kernel: one workgroup (4 wavefronts) is
+// one worker owning one sample at a time (Section III-A.1); every per-sample
+// value stays in LDS; conv1 forward (with the 2x2 pool fused into its
+// epilogue), conv2 forward, conv2 weight gradient and conv2 backward data are
+// implicit GEMMs on v_mfma_f32_16x16x4_f32; the 3x3 pool and the fully
+// connected layers run on the vector ALUs.  Per layer the partial derivatives
+// of the layer below are computed from the layer's weights before the layer's
+// gradient is pushed (Section III-A.2), lock-free (III-A.3).
+#include "chaos_internal.h"
+#include "device_common.h"
+
+namespace chaos {
+namespace {
+
+template <int C1_, int C2_, int F1_>
+struct Cpcp {
+    static constexpr int C1 = C1_, C2 = C2_, F1 = F1_, F2 = 10;
+    static constexpr int IN = 29, NX = IN * IN;
+    static constexpr int Q1 = 13, NP1 = Q1 * Q1;        // pool1 output 13x13
+    static constexpr int H2 = 9, NY2 = H2 * H2;         // conv2 output 9x9
+    static constexpr int NP2 = 9;                       // pool2 output 3x3
+    static constexpr int NF1 = C2 * NP2;                // FC1 inputs
+    static constexpr int KC2 = C1 * 25;                 // conv2 K = (c,u,v)
+    static constexpr int KC2P = (KC2 + 15) / 16 * 16;   // padded to whole tiles
+    static constexpr int KS2 = (KC2 + 3) / 4;           // conv2 forward k-steps
+    static constexpr int CT1 = (C1 + 15) / 16;          // conv1 col tiles
+    static constexpr int CT2 = (C2 + 15) / 16;          // conv2 map tiles
+    static constexpr int C2P = CT2 * 16;
+    static constexpr int OKS = (C2 + 3) / 4;            // k-steps over output maps
+    // canonical parameter offsets
+    static constexpr int OW1 = 0, OB1 = C1 * 16;
+    static constexpr int OW2 = OB1 + C1, OB2 = OW2 + C2 * KC2;
+    static constexpr int OF1 = OB2 + C2, OBF1 = OF1 + F1 * NF1;
+    static constexpr int OF2 = OBF1 + F1, OBF2 = OF2 + F2 * F1;
+    static constexpr int NPARAM = OBF2 + F2;
+};
+
+constexpr int NT = 256, NW = 4;
+constexpr int RT2 = 6;  // conv2 output positions 81 -> 6 tiles of 16
+
+template <class S>
+struct alignas(16) SmemCpcp {
+    float x[S::NX + 3];
+    float p1[S::C1 * S::NP1];            // pool1 output, later pool1 errors/deltas in e1
+    float e1[S::C1 * S::NP1];            // dE/d(pool1 output)
+    float y2[S::C2 * S::NY2];            // conv2 output
+    float d2[S::C2P * 96];               // conv2 output deltas (dense, zero off the argmax)
+    float p2[S::NF1], e2[S::NF1];        // pool2 output / its errors
+    float h[S::F1 + 16], dh[S::F1 + 16];
+    float o[16], dout[16];
+    alignas(16) int koff2[S::KC2P];      // im2col offset into p1 of k = (c,u,v)
+    unsigned char am1[S::C1 * S::NP1 + 16];
+    unsigned char am2[S::NF1 + 16];
+    int64_t idx;
+};
+
+template <class S, int MODE, int MINB>
+__global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
+    __shared__ SmemCpcp<S> sm;
+    const float *W = a.params;
+    constexpr bool kTrain = (MODE == kTrainAtomic || MODE == kTrainRacy);
+
+    for (int k = threadIdx.x; k < S::KC2P; k += NT) {
+        int c = k / 25, uv = k - 25 * c, u = uv / 5, v = uv - 5 * u;
+        sm.koff2[k] = (k < S::KC2) ? c * S::NP1 + u * S::Q1 + v : 0;
+    }
+
+    for (int64_t step = 0;; ++step) {
+        // opaque thread index: keeps per-phase index arithmetic inside its phase
+        int tid_l = threadIdx.x;
+        asm volatile("" : "+v"(tid_l));
+        const int tid = tid_l, lane = tid_l & 63, lr = lane & 15, lg = lane >> 4;
+        const int wave = __builtin_amdgcn_readfirstlane(tid_l >> 6);
+
+        if (tid == 0) sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1)
+                                      : (int64_t)blockIdx.x + step * gridDim.x;
+        __syncthreads();
+        const int64_t idx = sm.idx;
+        if (idx >= a.n) break;
+        if (kTrain) {
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+            if (a.claims && tid == 0) atomicAdd(a.claims + idx, 1);
+        }
+        const int label = a.labels[idx];
+        for (int i = tid; i < S::NX; i += NT) sm.x[i] = a.x[idx * S::NX + i];
+        __syncthreads();
+
+        // ---- conv1 + pool1: rows (P, w) P < 169, cols o < C1, K = 16 ----
+        {
+            float bw[4][S::CT1];
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int j = 0; j < S::CT1; ++j) {
+                    int o = 16 * j + lr;
+                    bw[s][j] = (o < S::C1) ? W[S::OW1 + o * 16 + 4 * s + lg] : 0.0f;
+                }
+            for (int i = wave; i < 43; i += NW) {
+                int m = 16 * i + lr, P = m >> 2;
+                bool valid = P < S::NP1;
+                int base = valid ? window_pos(P, m & 3, S::Q1, S::IN) : 0;
+                f4 acc[S::CT1];
+#pragma unroll
+                for (int j = 0; j < S::CT1; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    float av = valid ? sm.x[base + s * S::IN + lg] : 0.0f;
+#pragma unroll
+                    for (int j = 0; j < S::CT1; ++j) acc[j] = mfma(av, bw[s][j], acc[j]);
+                }
+                int Pe = 4 * i + lg;
+                if (Pe < S::NP1) {
+#pragma unroll
+                    for (int j = 0; j < S::CT1; ++j) {
+                        int o = 16 * j + lr;
+                        if (o < S::C1) {
+                            float ym;
+                            int ag;
+                            pool4(acc[j], W[S::OB1 + o], ym, ag);
+                            sm.p1[o * S::NP1 + Pe] = ym;
+                            sm.am1[o * S::NP1 + Pe] = (unsigned char)ag;
+                        }
+                    }
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- conv2: rows p < 81 (6 tiles), cols o < C2, K = C1*25 ----
+        for (int i = wave; i < RT2; i += NW) {
+            f4 acc[S::CT2];
+#pragma unroll
+            for (int j = 0; j < S::CT2; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+            int p = 16 * i + lr;
+            bool pv = p < S::NY2;
+            int py = p / S::H2, px = p - py * S::H2;
+            int base = pv ? py * S::Q1 + px : 0;
+            float bA[S::CT2], bB[S::CT2];
+            auto load_b = [&](float (&b)[S::CT2], int ks) {
+                int k = 4 * ks + lg;
+#pragma unroll
+                for (int j = 0; j < S::CT2; ++j) {
+                    int o = 16 * j + lr;
+                    b[j] = (o < S::C2 && k < S::KC2) ? W[S::OW2 + o * S::KC2 + k] : 0.0f;
+                }
+            };
+            auto compute = [&](const float (&b)[S::CT2], int ks) {
+                int k = 4 * ks + lg;
+                float av = (pv && k < S::KC2) ? sm.p1[base + sm.koff2[k]] : 0.0f;
+#pragma unroll
+                for (int j = 0; j < S::CT2; ++j) acc[j] = mfma(av, b[j], acc[j]);
+            };
+            load_b(bA, 0);
+            for (int ks = 0; ks < S::KS2; ks += 2) {
+                if (ks + 1 < S::KS2) load_b(bB, ks + 1);
+                compute(bA, ks);
+                if (ks + 1 < S::KS2) {
+                    if (ks + 2 < S::KS2) load_b(bA, ks + 2);
+                    compute(bB, ks + 1);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < S::CT2; ++j) {
+                int o = 16 * j + lr;
+                if (o >= S::C2) continue;
+                float bias = W[S::OB2 + o];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    int pe = 16 * i + 4 * lg + r;
+                    if (pe < S::NY2) sm.y2[o * S::NY2 + pe] = act_y(acc[j][r] + bias);
+                }
+            }
+        }
+        __syncthreads();
+
+        // ---- pool2: 3x3 windows of the 9x9 maps, first maximum wins ----
+        for (int t = tid; t < S::NF1; t += NT) {
+            int o = t / S::NP2, P = t - o * S::NP2;
+            int py = P / 3, px = P - 3 * py;
+            const float *yo = sm.y2 + o * S::NY2 + 3 * py * S::H2 + 3 * px;
+            float m = yo[0];
+            int ag = 0;
+#pragma unroll
+            for (int w = 1; w < 9; ++w) {
+                float v = yo[(w / 3) * S::H2 + (w % 3)];
+                if (v > m) { m = v; ag = w; }
+            }
+            sm.p2[t] = m;
+            sm.am2[t] = (unsigned char)ag;
+        }
+        __syncthreads();
+
+        // ---- FC1 and FC2 (one wavefront per neuron, lanes over inputs) ----
+        {
+            constexpr int IT = (S::NF1 + 63) / 64;
+            for (int j0 = 4 * wave; j0 < S::F1; j0 += 4 * NW) {
+                float wv[4][IT];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int it = 0; it < IT; ++it) {
+                        int j = j0 + q, i = lane + 64 * it;
+                        wv[q][it] = (j < S::F1 && i < S::NF1) ? W[S::OF1 + j * S::NF1 + i] : 0.0f;
+                    }
+                float s[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int it = 0; it < IT; ++it) {
+                    int i = lane + 64 * it;
+                    float xi = (i < S::NF1) ? sm.p2[i] : 0.0f;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) s[q] = fmaf(wv[q][it], xi, s[q]);
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    float t = wave_sum(s[q]);
+                    if (lane == 0 && j0 + q < S::F1) sm.h[j0 + q] = act_y(t + W[S::OBF1 + j0 + q]);
+                }
+            }
+        }
+        __syncthreads();
+        for (int j = wave; j < S::F2; j += NW) {
+            float s = 0.0f;
+#pragma unroll
+            for (int it = 0; it < (S::F1 + 63) / 64; ++it) {
+                int i = lane + 64 * it;
+                if (i < S::F1) s = fmaf(W[S::OF2 + j * S::F1 + i], sm.h[i], s);
+            }
+            s = wave_sum(s);
+            if (lane == 0) sm.o[j] = act_y(s + W[S::OBF2 + j]);
+        }
+        __syncthreads();
+        if (a.out && tid < S::F2) a.out[idx * S::F2 + tid] = sm.o[tid];
+
+        if (MODE == kEvaluate) {
+            if (tid == 0) {
+                int best = 0;
+                for (int k = 1; k < S::F2; ++k)
+                    if (sm.o[k] > sm.o[best]) best = k;
+                if (best != label) atomicAdd(a.n_wrong, 1);
+            }
+            __syncthreads();
+            continue;
+        }
+
+        // ================= back-propagation =================
+        Push push;
+        push.mode = MODE;
+        push.params = a.params;
+        push.neg_lr = -a.lr;
+        push.each = a.grad_each ? a.grad_each + idx * (int64_t)S::NPARAM : nullptr;
+        push.part = a.grad_part ? a.grad_part + (int64_t)blockIdx.x * S::NPARAM : nullptr;
+
+        if (tid < 64) {
+            float e = 0.0f;
+            if (tid < S::F2) {
+                float y = sm.o[tid];
+                float d = y - (tid == label ? 1.0f : 0.0f);
+                e = d * d;
+                sm.dout[tid] = d * dact_from_y(y);
+            }
+            e = wave_sum(e);
+            if (tid == 0 && a.loss) a.loss[idx] = 0.5f * e;
+        }
+        __syncthreads();
+        // FC2 backward data (pre-update weights)
+        for (int i = tid; i < S::F1; i += NT) {
+            float wv[S::F2];
+#pragma unroll
+            for (int j = 0; j < S::F2; ++j) wv[j] = W[S::OF2 + j * S::F1 + i];
+            float s = 0.0f;
+#pragma unroll
+            for (int j = 0; j < S::F2; ++j) s = fmaf(wv[j], sm.dout[j], s);
+            sm.dh[i] = s * dact_from_y(sm.h[i]);
+        }
+        __syncthreads();
+        // FC2 push; FC1 backward data (pre-update weights)
+        for (int t = tid; t < S::F2 * S::F1; t += NT) {
+            int j = t / S::F1, i = t - j * S::F1;
+            push(S::OF2 + t, sm.dout[j] * sm.h[i]);
+        }
+        if (tid < S::F2) push(S::OBF2 + tid, sm.dout[tid]);
+        for (int i = tid; i < S::NF1; i += NT) {
+            float s = 0.0f;
+            for (int j0 = 0; j0 < S::F1; j0 += 10) {
+                float wv[10];
+#pragma unroll
+                for (int jj = 0; jj < 10; ++jj)
+                    wv[jj] = (j0 + jj < S::F1) ? W[S::OF1 + (j0 + jj) * S::NF1 + i] : 0.0f;
+#pragma unroll
+                for (int jj = 0; jj < 10; ++jj)
+                    if (j0 + jj < S::F1) s = fmaf(wv[jj], sm.dh[j0 + jj], s);
+            }
+            sm.e2[i] = s;
+        }
+        __syncthreads();
+        // FC1 push; pool2 backward -> dense conv2 deltas; clear e1
+        for (int t = tid; t < S::F1 * S::NF1; t += NT) {
+            int j = t / S::NF1, i = t - j * S::NF1;
+            push(S::OF1 + t, sm.dh[j] * sm.p2[i]);
+        }
+        if (tid < S::F1) push(S::OBF1 + tid, sm.dh[tid]);
+        for (int t = tid; t < S::C2P * 96; t += NT) {
+            int o = t / 96, p = t - 96 * o;
+            float d = 0.0f;
+            if (o < S::C2 && p < S::NY2) {
+                int py = p / S::H2, px = p - py * S::H2;
+                int q = o * S::NP2 + (py / 3) * 3 + px / 3;
+                int w = (py % 3) * 3 + px % 3;
+                if (sm.am2[q] == w) d = sm.e2[q] * dact_from_y(sm.p2[q]);
+            }
+            sm.d2[t] = d;
+        }
+        for (int t = tid; t < S::C1 * S::NP1; t += NT) sm.e1[t] = 0.0f;
+        __syncthreads();
+
+        // ---- conv2 backward data: C[(c,u,v)][p] = sum_o W2[o][c][u][v] d2[o][p],
+        //      col2im into e1[c][p + (u,v)].  Wavefront w owns input maps
+        //      c = w, w+4, ... (25 rows each, 2 tiles), so the LDS adds into a
+        //      map come from one wavefront in program order: reproducible. ----
+        for (int c = wave; c < S::C1; c += NW) {
+            f4 acc[2][RT2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+            for (int ks = 0; ks < S::OKS; ++ks) {
+                int o = 4 * ks + lg;
+                float av[2], bv[RT2];
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    int uv = 16 * t + lr;
+                    av[t] = (o < S::C2 && uv < 25) ? W[S::OW2 + o * S::KC2 + c * 25 + uv] : 0.0f;
+                }
+#pragma unroll
+                for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
+            }
+            float *ec = sm.e1 + c * S::NP1;
+#pragma unroll
+            for (int j = 0; j < RT2; ++j) {
+                int p = 16 * j + lr;
+                if (p >= S::NY2) continue;
+                int py = p / S::H2, px = p - py * S::H2;
+                float *ep = ec + py * S::Q1 + px;
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        int uv = 16 * t + 4 * lg + r;
+                        int u = uv / 5, v = uv - 5 * u;
+                        if (uv < 25)
+                            __hip_atomic_fetch_add(ep + u * S::Q1 + v, acc[t][j][r], __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_WORKGROUP);
+                    }
+            }
+        }
+        __syncthreads();
+
+        // ---- conv2 weight gradient: G[o][k] = sum_p d2[o][p] p1col[p][k], pushed;
+        //      pool1 backward: delta at each window's maximum ----
+        {
+            float ad[S::CT2][21];
+#pragma unroll
+            for (int i = 0; i < S::CT2; ++i)
+#pragma unroll
+                for (int s = 0; s < 21; ++s) ad[i][s] = sm.d2[(16 * i + lr) * 96 + 4 * s + lg];
+            int pb[21];
+#pragma unroll
+            for (int s = 0; s < 21; ++s) {
+                int p = 4 * s + lg;
+                int py = p / S::H2, px = p - py * S::H2;
+                pb[s] = (p < S::NY2) ? py * S::Q1 + px : -1;
+            }
+            for (int jt = wave; jt < S::KC2P / 16; jt += NW) {
+                int k = 16 * jt + lr;
+                bool kv = k < S::KC2;
+                const float *pc = sm.p1 + (kv ? sm.koff2[k] : 0);
+                f4 acc[S::CT2];
+#pragma unroll
+                for (int i = 0; i < S::CT2; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int s = 0; s < 21; ++s) {
+                    float bv = (kv && pb[s] >= 0) ? pc[pb[s]] : 0.0f;
+#pragma unroll
+                    for (int i = 0; i < S::CT2; ++i) acc[i] = mfma(ad[i][s], bv, acc[i]);
+                }
+                if (kv) {
+#pragma unroll
+                    for (int i = 0; i < S::CT2; ++i)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            int o = 16 * i + 4 * lg + r;
+                            if (o < S::C2) push(S::OW2 + o * S::KC2 + k, acc[i][r]);
+                        }
+                }
+            }
+            if (tid < S::C2) {
+                float g = 0.0f;
+#pragma unroll 8
+                for (int p = 0; p < S::NY2; ++p) g += sm.d2[tid * 96 + p];
+                push(S::OB2 + tid, g);
+            }
+            for (int t = tid; t < S::C1 * S::NP1; t += NT) sm.e1[t] *= dact_from_y(sm.p1[t]);
+        }
+        __syncthreads();
+
+        // ---- conv1 weight gradient from the pool1 deltas at each window's maximum ----
+        for (int t = tid; t < S::C1 * 16 + S::C1; t += NT) {
+            float g = 0.0f;
+            if (t < S::C1 * 16) {
+                int o = t >> 4, u = (t >> 2) & 3, v = t & 3;
+                const float *d1 = sm.e1 + o * S::NP1;
+                const unsigned char *am = sm.am1 + o * S::NP1;
+                const float *xs = sm.x + u * S::IN + v;
+                for (int py = 0; py < S::Q1; ++py)
+#pragma unroll
+                    for (int px = 0; px < S::Q1; ++px) {
+                        int P = py * S::Q1 + px, w = am[P];
+                        g = fmaf(d1[P], xs[(2 * py + (w >> 1)) * S::IN + 2 * px + (w & 1)], g);
+                    }
+                push(S::OW1 + t, g);
+            } else {
+                int o = t - S::C1 * 16;
+#pragma unroll 8
+                for (int P = 0; P < S::NP1; ++P) g += sm.e1[o * S::NP1 + P];
+                push(S::OB1 + o, g);
+            }
+        }
+        __syncthreads();
+    }
+}
+
+using Small = Cpcp<5, 10, 50>;
+using Medium = Cpcp<20, 40, 150>;
+static_assert(Small::NPARAM == 6405 && Medium::NPARAM == 76040, "Table I weight counts");
+
+template <class S, int MINB>
+hipError_t launch_cpcp(int mode, const WorkArgs &a, int grid, hipStream_t s) {
+    switch (mode) {
+    case kTrainAtomic: fused_cpcp_kernel<S, kTrainAtomic, MINB><<<grid, NT, 0, s>>>(a); break;
+    case kTrainRacy: fused_cpcp_kernel<S, kTrainRacy, MINB><<<grid, NT, 0, s>>>(a); break;
+    case kForwardBackward: fused_cpcp_kernel<S, kForwardBackward, MINB><<<grid, NT, 0, s>>>(a); break;
+    case kEvaluate: fused_cpcp_kernel<S, kEvaluate, MINB><<<grid, NT, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <class S, int MINB>
+int cpcp_blocks_per_cu() {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &nb, fused_cpcp_kernel<S, kTrainAtomic, MINB>, NT, 0) != hipSuccess)
+        return 0;
+    return nb;
+}
+
+constexpr int kSmallMinBlocks = 2, kMediumMinBlocks = 2;
+
+bool matches(const Net &net, int c1, int c2, int f1) {
+    const int spec[6][3] = {{kConv, c1, 4}, {kPool, 0, 2}, {kConv, c2, 5},
+                            {kPool, 0, 3},  {kFc, f1, 0},  {kFc, 10, 0}};
+    if (net.n_layers != 6 || net.in_size != 29 * 29) return false;
+    if (net.L[0].hin != 29 || net.L[0].win != 29) return false;
+    for (int l = 0; l < 6; ++l) {
+        const Layer &ly = net.L[l];
+        if (ly.kind != spec[l][0]) return false;
+        if (ly.kind != kFc && ly.k != spec[l][2]) return false;
+        if (ly.kind != kPool && ly.cout != spec[l][1]) return false;
+    }
+    return true;
+}
+
+} // namespace
+
+int fused_cpcp_variant(const Net &net) {
+    if (matches(net, Small::C1, Small::C2, Small::F1)) return 1;
+    if (matches(net, Medium::C1, Medium::C2, Medium::F1)) return 2;
+    return 0;
+}
+
+hipError_t launch_fused_cpcp(int variant, int mode, const WorkArgs &a, int grid, hipStream_t s) {
+    if (variant == 1) return launch_cpcp<Small, kSmallMinBlocks>(mode, a, grid, s);
+    if (variant == 2) return launch_cpcp<Medium, kMediumMinBlocks>(mode, a, grid, s);
+    return hipErrorInvalidValue;
+}
+
+int fused_cpcp_blocks_per_cu(int variant) {
+    if (variant == 1) return cpcp_blocks_per_cu<Small, kSmallMinBlocks>();
+    if (variant == 2) return cpcp_blocks_per_cu<Medium, kMediumMinBlocks>();
+    return 0;
+}
+
+} // namespace chaos

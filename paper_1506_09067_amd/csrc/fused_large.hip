@@ -26,12 +26,6 @@
 namespace chaos {
 namespace {
 
-typedef float f4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ f4 mfma(float a, float b, f4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
 // ---- shapes of the large net ---------------------------------------------
 constexpr int IN = 29, NX = IN * IN;            // input 1x29x29
 constexpr int C1 = 20, K1 = 4, Q1 = 13;         // conv1 20@26x26, pool -> 13x13
@@ -84,50 +78,18 @@ struct alignas(16) Smem {
 };
 static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
 
-// scaled tanh without its derivative (forward epilogues)
-__device__ __forceinline__ float act_y(float z) {
-    float y, d;
-    activation(z, y, d);
-    return y;
-}
-
-// f'(z) from y = f(z): A B (1 - (y/A)^2) = (B/A)(A^2 - y^2)
-__device__ __forceinline__ float dact_from_y(float y) {
-    return (kActB / kActA) * (kActA * kActA - y * y);
-}
-
-// Max over a 2x2 window held in one lane's accumulator (window elements in
-// row-major order); the first maximum wins.
-__device__ __forceinline__ void pool4(f4 acc, float bias, float &ymax, int &arg) {
-    ymax = act_y(acc[0] + bias);
-    arg = 0;
-#pragma unroll
-    for (int r = 1; r < 4; ++r) {
-        float y = act_y(acc[r] + bias);
-        if (y > ymax) { ymax = y; arg = r; }
-    }
-}
-
-// position (row-major index into a map of width `wd`) of element w of the
-// 2x2 window of pooled position P on a pooled grid of width `pw`
-__device__ __forceinline__ int window_pos(int P, int w, int pw, int wd) {
-    int py = P / pw, px = P - py * pw;
-    return (2 * py + (w >> 1)) * wd + 2 * px + (w & 1);
-}
-
 template <int MODE>
 __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
     __shared__ Smem sm;
-    const int tid = threadIdx.x;
     const float *W = a.params;
     constexpr bool kTrain = (MODE == kTrainAtomic || MODE == kTrainRacy);
 
     // sample-invariant im2col offset tables
-    for (int k = tid; k < KC3; k += NT) {
+    for (int k = threadIdx.x; k < KC3; k += NT) {
         int c = k / 36, uv = k - 36 * c, u = uv / 6, v = uv - 6 * u;
         sm.koff3[k] = c * NY2 + u * H2 + v;
     }
-    for (int k = tid; k < KC2 + 4; k += NT) {
+    for (int k = threadIdx.x; k < KC2 + 4; k += NT) {
         int c = k / 9, uv = k - 9 * c, u = uv / 3, v = uv - 3 * u;
         sm.koff2[k] = (k < KC2) ? c * NP1 + u * Q1 + v : 0;
     }
@@ -138,7 +100,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         // instead of being hoisted out of this loop and kept live throughout.
         int tid_l = threadIdx.x;
         asm volatile("" : "+v"(tid_l));
-        const int lane = tid_l & 63, lr = lane & 15, lg = lane >> 4;
+        const int tid = tid_l, lane = tid_l & 63, lr = lane & 15, lg = lane >> 4;
         const int wave = __builtin_amdgcn_readfirstlane(tid_l >> 6);
         // ---- claim a sample (Section III-A.1) ----
         if (tid == 0) sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1)

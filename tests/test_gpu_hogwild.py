@@ -49,8 +49,9 @@ def _train_and_test(torch, chaos, name, x, y, xt, yt, epochs, lr, decay, mode, w
 # every worker at lr 5e-4 (no spike in 16 runs each).
 CASES = [
     ("small", 20000, 3, 1e-3, 256),
-    ("large", 20000, 1, 1e-3, 64),
-    ("large", 20000, 1, 5e-4, 0),
+    ("medium", 60000, 1, 1e-3, 128),
+    ("large", 60000, 1, 1e-3, 64),
+    ("large", 60000, 1, 5e-4, 0),
 ]
 
 
@@ -58,7 +59,7 @@ CASES = [
 def test_hogwild_matches_sequential_sgd(env, name, n, epochs, lr, workers):
     torch, chaos = env
     x, y = wl.train_set(n)
-    xt, yt = wl.test_set(5000)
+    xt, yt = wl.test_set(10000)
     decay = 0.9
     seq = _train_and_test(torch, chaos, name, x, y, xt, yt, epochs, lr, decay, chaos.SEQUENTIAL, 0)
     hog = _train_and_test(torch, chaos, name, x, y, xt, yt, epochs, lr, decay,

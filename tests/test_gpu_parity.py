@@ -98,9 +98,10 @@ def test_grad_sum_ragged_batch(chaos, torch_cuda, name, n):
     assert_close(gsum.cpu().numpy(), G, what="grad_sum")
 
 
-def test_grad_sum_bitwise_reproducible(chaos, torch_cuda):
+@pytest.mark.parametrize("name", ["small", "medium", "large", "large_table1"])
+def test_grad_sum_bitwise_reproducible(chaos, torch_cuda, name):
     torch = torch_cuda
-    net, layers, p = _net(chaos, "large")
+    net, layers, p = _net(chaos, name)
     x, y = wl.batch_set(700)
     xd, yd = _dev(torch, x, torch.float32), _dev(torch, y, torch.int32)
     g1 = torch.empty(net.n_params, device="cuda")
@@ -155,14 +156,15 @@ def test_sequential_sgd_tiny_run(chaos, torch_cuda):
         assert norm <= 1e-3, f"weights after 1000 samples ({amb.size} ambiguous): {msg}"
 
 
-def test_hogwild_one_worker_is_sequential(chaos, torch_cuda):
+@pytest.mark.parametrize("name", ["small", "medium", "large", "large_table1"])
+def test_hogwild_one_worker_is_sequential(chaos, torch_cuda, name):
     torch = torch_cuda
-    x, y = wl.train_set(600)
+    x, y = wl.train_set(300)
     xd, yd = _dev(torch, x, torch.float32), _dev(torch, y, torch.int32)
     res = []
     for mode, workers in ((chaos.SEQUENTIAL, 0), (chaos.HOGWILD_ATOMIC, 1), (chaos.HOGWILD_RACY, 1)):
-        net, _, _ = _net(chaos, "medium")
-        loss = torch.empty(600, device="cuda")
+        net, _, _ = _net(chaos, name)
+        loss = torch.empty(300, device="cuda")
         net.train_epoch(xd, yd, 1e-3, mode=mode, workers=workers, loss=loss)
         res.append((net.get_params().cpu(), loss.cpu()))
     for name, (w, l) in zip(("atomic", "racy"), res[1:]):
