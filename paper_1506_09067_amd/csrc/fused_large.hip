@@ -70,6 +70,7 @@ struct alignas(16) Smem {
     float e3[NF1];                       // dE/d(pool2 output)
     float h[F1 + 10], dh[F1 + 10];
     float o[16], dout[16];
+    float pushbuf[NW][16 * 65];          // per-wavefront transpose of a 16 x 64 gradient block
     alignas(16) int koff3[KC3];          // im2col offset into y2 of k = (c,u,v), conv3
     alignas(16) int koff2[KC2 + 4];      // im2col offset into p1 of k = (c,u,v), conv2
     unsigned char am1[C1 * NP1 + 12];    // pool1 argmax (window element 0..3)
@@ -461,9 +462,8 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         // same s2 entries.  Row q of tile i holds input map c0 + q/4 at kernel
         // offset uv = 4i + q%4: in the accumulator the four lane groups then
         // hold four different maps at one (u,v), so no scatter instruction
-        // has two lanes on one address.  Different instructions do meet
-        // (lanes are threads: those adds are LDS atomics).  The next output
-        // map's weights are loaded while the current one computes.
+        // has two lanes on one address.  The next output map's weights are
+        // loaded while the current one computes.
         for (int blk = wave; blk < C2 / 4; blk += NW) {
             f4 acc[9][3];
 #pragma unroll
@@ -497,21 +497,28 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     compute(aB, ks + 1);
                 }
             }
+            // scatter grouped by kernel offset uv: inside a group the 3 x 64
+            // lanes write distinct addresses; the fence (an LDS wait) orders
+            // the groups, whose targets overlap
             float *dst = sm.s2 + (4 * blk + lg) * NY2;
+            float *dm[3];
+            bool mv[3];
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
                 int m = 16 * j + lr;
-                if (m >= M3) continue;
-                float *dm = dst + window_pos(m >> 2, m & 3, 3, H2);
-#pragma unroll
-                for (int i = 0; i < 9; ++i)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int uv = 4 * i + r, u = uv / 6, v = uv - 6 * u;
-                        __hip_atomic_fetch_add(dm + u * H2 + v, acc[i][j][r], __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_WORKGROUP);
-                    }
+                mv[j] = m < M3;
+                dm[j] = dst + (mv[j] ? window_pos(m >> 2, m & 3, 3, H2) : 0);
             }
+#pragma unroll
+            for (int i = 0; i < 9; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int uv = 4 * i + r, u = uv / 6, v = uv - 6 * u;
+#pragma unroll
+                    for (int j = 0; j < 3; ++j)
+                        if (mv[j]) dm[j][u * H2 + v] += acc[i][j][r];
+                    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+                }
         }
         __syncthreads();
 
@@ -525,26 +532,46 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     int o = 16 * i + lr;
                     ad[i][s] = (o < C3) ? sm.d3[o * M3P + 4 * s + lg] : 0.0f;
                 }
-            for (int jt = wave; jt < KC3 / 16; jt += NW) {
-                int k = 16 * jt + lr;
-                const float *ycol = sm.y2 + sm.koff3[k];
-                f4 acc[7];
+            // four adjacent column tiles (64 consecutive k) per step; each
+            // 16 x 64 block is transposed through LDS so that every push
+            // instruction covers 64 consecutive weights of one output map
+            // (256 contiguous bytes)
+            float *pb = sm.pushbuf[wave];
+            for (int grp = wave; grp < (KC3 / 16 + 3) / 4; grp += NW) {
+                f4 acc[4][7];
 #pragma unroll
-                for (int i = 0; i < 7; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+                for (int t = 0; t < 4; ++t)
 #pragma unroll
-                for (int s = 0; s < 9; ++s) {
-                    int m = 4 * s + lg;
-                    float bv = ycol[window_pos(m >> 2, m & 3, 3, H2)];
+                    for (int i = 0; i < 7; ++i) acc[t][i] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int i = 0; i < 7; ++i) acc[i] = mfma(ad[i][s], bv, acc[i]);
-                }
+                for (int t = 0; t < 4; ++t) {
+                    const int k = 64 * grp + 16 * t + lr;
+                    if (64 * grp + 16 * t >= KC3) continue;
+                    const float *ycol = sm.y2 + sm.koff3[k];
 #pragma unroll
-                for (int i = 0; i < 7; ++i)
+                    for (int s9 = 0; s9 < 9; ++s9) {
+                        int m = 4 * s9 + lg;
+                        float bv = ycol[window_pos(m >> 2, m & 3, 3, H2)];
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        int o = 16 * i + 4 * lg + r;
-                        if (o < C3) push(OW3 + o * KC3 + k, acc[i][r]);
+                        for (int i = 0; i < 7; ++i) acc[t][i] = mfma(ad[i][s9], bv, acc[t][i]);
                     }
+                }
+                const int kb = 64 * grp + lane;
+#pragma unroll
+                for (int i = 0; i < 7; ++i) {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) pb[(4 * lg + r) * 65 + 16 * t + lr] = acc[t][i][r];
+                    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+#pragma unroll
+                    for (int row = 0; row < 16; ++row) {
+                        int o = 16 * i + row;
+                        float g = pb[row * 65 + lane];
+                        if (o < C3 && kb < KC3) push(OW3 + o * KC3 + kb, g);
+                    }
+                    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+                }
             }
             if (tid < C3) {
                 float g = 0.0f;
@@ -610,24 +637,34 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     compute(aB, ks + 1);
                 }
             }
+            // tiles 0..2: scatter grouped by kernel offset uv (distinct
+            // addresses inside a group, groups ordered by an LDS wait);
+            // tile 3 (one map, lanes at different uv may meet): LDS atomics
             float *e1 = sm.s2;
+            float *dp[8];
+            bool pv[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 int p = 16 * j + lr;
-                if (p >= NY2) continue;
+                pv[j] = p < NY2;
                 int py = p / H2, px = p - py * H2;
-                float *dp = e1 + py * Q1 + px;
-                float *dm = dp + (c0 + lg) * NP1;
+                dp[j] = e1 + (pv[j] ? py * Q1 + px : 0);
+            }
 #pragma unroll
-                for (int i = 0; i < 3; ++i)
+            for (int i = 0; i < 3; ++i)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int uv = 4 * i + r, u = uv / 3, v = uv - 3 * u;
-                        if (uv < 9)
-                            __hip_atomic_fetch_add(dm + u * Q1 + v, acc[i][j][r], __ATOMIC_RELAXED,
-                                                   __HIP_MEMORY_SCOPE_WORKGROUP);
-                    }
-                float *d4 = dp + (c0 + 4) * NP1;
+                for (int r = 0; r < 4; ++r) {
+                    const int uv = 4 * i + r, u = uv / 3, v = uv - 3 * u;
+                    if (uv >= 9) continue;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        if (pv[j]) dp[j][(c0 + lg) * NP1 + u * Q1 + v] += acc[i][j][r];
+                    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+                }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                if (!pv[j]) continue;
+                float *d4 = dp[j] + (c0 + 4) * NP1;
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     int uv = 4 * lg + r, u = uv / 3, v = uv - 3 * u;
