@@ -130,6 +130,24 @@ int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_
 int chaos_evaluate(chaos_net *net, const float *x_dev, const int32_t *labels_dev, int64_t n,
                    float *out_dev, int32_t *n_wrong_dev, hipStream_t stream);
 
+/* A training session (Section III-A.1): for each epoch e = 0..epochs-1,
+ * Training over x_train[0..n_train) (as chaos_train_epoch, with
+ * lr = lr0 * decay^e computed in double and rounded to float), then
+ * Validation on the training set and Testing on x_test[0..n_test) (forward
+ * only, as chaos_evaluate).  stats_dev [epochs][4] floats receives per epoch:
+ *   [0] mean training loss (each sample's loss when it was processed)
+ *   [1] wrong predictions on the training set after the epoch (Validation)
+ *   [2] wrong predictions on the test set (Testing, the Table II count)
+ *   [3] mean test loss
+ * n_test may be 0 (then [2] and [3] are 0).  Uses net-owned buffers of
+ * n_train and n_test floats, allocated on first use (the only call here that
+ * may allocate device memory after chaos_create_net, together with the batch
+ * gradient's partial sums). */
+int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t *labels_train_dev,
+                        int64_t n_train, const float *x_test_dev, const int32_t *labels_test_dev,
+                        int64_t n_test, int32_t epochs, float lr0, float decay, int32_t mode,
+                        int32_t workers, float *stats_dev, hipStream_t stream);
+
 /* Largest number of concurrent Hogwild workers the device keeps resident. */
 int32_t chaos_max_workers(const chaos_net *net);
 

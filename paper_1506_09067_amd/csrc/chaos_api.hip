@@ -5,6 +5,7 @@
 #include "chaos_internal.h"
 
 #include <algorithm>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -27,6 +28,9 @@ struct chaos_net {
     int fb_workers = 0;           // rows of grad_part
     float *grad_part = nullptr;   // [fb_workers][n_params]
     int32_t *claims = nullptr;    // debug claim counter (caller-owned)
+    float *sess_loss = nullptr;   // session: per-sample losses (training, then test)
+    int64_t sess_loss_n = 0;
+    int32_t *sess_wrong = nullptr;
 };
 
 namespace {
@@ -238,6 +242,8 @@ int chaos_destroy_net(chaos_net *net) {
     (void)hipFree(net->scratch);
     (void)hipFree(net->counter);
     (void)hipFree(net->grad_part);
+    (void)hipFree(net->sess_loss);
+    (void)hipFree(net->sess_wrong);
     delete net;
     return ok();
 }
@@ -357,6 +363,55 @@ int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *la
         HIP_TRY(chaos::launch_reduce_partials(net->grad_part, grid, net->n_params, grad_sum_dev,
                                               stream),
                 "reduce");
+    return ok();
+}
+
+int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t *labels_train_dev,
+                        int64_t n_train, const float *x_test_dev, const int32_t *labels_test_dev,
+                        int64_t n_test, int32_t epochs, float lr0, float decay, int32_t mode,
+                        int32_t workers, float *stats_dev, hipStream_t stream) {
+    if (int rc = check_net(net)) return rc;
+    if (int rc = check_io(x_train_dev, labels_train_dev, n_train)) return rc;
+    if (int rc = check_io(x_test_dev, labels_test_dev, n_test)) return rc;
+    if (epochs < 0) return fail(CHAOS_EINVAL, "epochs=%d < 0", epochs);
+    if (epochs > 0 && !stats_dev) return fail(CHAOS_EINVAL, "stats_dev is NULL");
+    if (mode != CHAOS_SEQUENTIAL && mode != CHAOS_HOGWILD_ATOMIC && mode != CHAOS_HOGWILD_RACY)
+        return fail(CHAOS_EINVAL, "unknown mode %d", mode);
+    if (workers < 0 || workers > net->max_workers)
+        return fail(CHAOS_EINVAL, "workers=%d outside [0,%d]", workers, net->max_workers);
+    if (int rc = set_device(net)) return rc;
+    const int64_t need = std::max<int64_t>(std::max(n_train, n_test), 1);
+    if (need > net->sess_loss_n) {
+        (void)hipFree(net->sess_loss);
+        net->sess_loss = nullptr;
+        net->sess_loss_n = 0;
+        if (hipMalloc(&net->sess_loss, (size_t)need * sizeof(float)) != hipSuccess)
+            return fail(CHAOS_ENOMEM, "session loss buffer");
+        net->sess_loss_n = need;
+    }
+    if (!net->sess_wrong && hipMalloc(&net->sess_wrong, 64) != hipSuccess)
+        return fail(CHAOS_ENOMEM, "session counter");
+    for (int32_t e = 0; e < epochs; ++e) {
+        float lr = (float)((double)lr0 * std::pow((double)decay, (double)e));
+        float *st = stats_dev + 4 * (int64_t)e;
+        int rc = chaos_train_epoch(net, x_train_dev, labels_train_dev, n_train, lr, mode, workers,
+                                   n_train ? net->sess_loss : nullptr, stream);
+        if (rc) return rc;
+        HIP_TRY(chaos::launch_mean(net->sess_loss, n_train, st + 0, stream), "session mean");
+        if ((rc = chaos_evaluate(net, x_train_dev, labels_train_dev, n_train, nullptr,
+                                 net->sess_wrong, stream)))
+            return rc;
+        HIP_TRY(chaos::launch_count(net->sess_wrong, st + 1, stream), "session count");
+        if ((rc = chaos_evaluate(net, x_test_dev, labels_test_dev, n_test, nullptr,
+                                 net->sess_wrong, stream)))
+            return rc;
+        HIP_TRY(chaos::launch_count(net->sess_wrong, st + 2, stream), "session count");
+        if (n_test > 0 &&
+            (rc = chaos_forward_backward(net, x_test_dev, labels_test_dev, n_test, nullptr,
+                                         net->sess_loss, nullptr, nullptr, stream)))
+            return rc;
+        HIP_TRY(chaos::launch_mean(net->sess_loss, n_test, st + 3, stream), "session mean");
+    }
     return ok();
 }
 

@@ -61,6 +61,8 @@ hipError_t launch_fill_f32(float *p, float v, int64_t n, hipStream_t s);
 hipError_t launch_reduce_partials(const float *part, int64_t rows, int64_t cols, float *dst,
                                   hipStream_t s);
 hipError_t launch_axpy(float *w, const float *g, float alpha, int64_t n, hipStream_t s);
+hipError_t launch_mean(const float *v, int64_t n, float *dst, hipStream_t s);
+hipError_t launch_count(const int32_t *src, float *dst, hipStream_t s);
 // Occupancy of the worker kernel: resident blocks per CU for a given block size.
 int worker_blocks_per_cu(int block);
 

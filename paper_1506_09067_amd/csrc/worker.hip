@@ -286,6 +286,26 @@ __global__ void reduce_partials_kernel(const float *__restrict__ part, int64_t r
     dst[c] = s;
 }
 
+// dst[0] = mean of v[0..n) in a fixed order: thread t sums t, t+1024, ...
+// sequentially, then a fixed tree over the 1024 partial sums.
+__global__ void __launch_bounds__(1024) mean_kernel(const float *__restrict__ v, int64_t n,
+                                                    float *__restrict__ dst) {
+    __shared__ float part[1024];
+    float s = 0.0f;
+    for (int64_t i = threadIdx.x; i < n; i += 1024) s += v[i];
+    part[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 512; h > 0; h >>= 1) {
+        if ((int)threadIdx.x < h) part[threadIdx.x] += part[threadIdx.x + h];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) dst[0] = n > 0 ? part[0] / (float)n : 0.0f;
+}
+
+__global__ void count_kernel(const int32_t *__restrict__ src, float *__restrict__ dst) {
+    if (threadIdx.x == 0) dst[0] = (float)src[0];
+}
+
 __global__ void axpy_kernel(float *__restrict__ w, const float *__restrict__ g, float alpha,
                             int64_t n) {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -324,6 +344,16 @@ hipError_t launch_reduce_partials(const float *part, int64_t rows, int64_t cols,
                                   hipStream_t s) {
     if (cols <= 0) return hipSuccess;
     reduce_partials_kernel<<<blocks_for(cols, 256), 256, 0, s>>>(part, rows, cols, dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_mean(const float *v, int64_t n, float *dst, hipStream_t s) {
+    mean_kernel<<<1, 1024, 0, s>>>(v, n, dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_count(const int32_t *src, float *dst, hipStream_t s) {
+    count_kernel<<<1, 64, 0, s>>>(src, dst);
     return hipGetLastError();
 }
 

@@ -312,3 +312,36 @@ def test_full_size_hogwild_epoch(chaos, torch_cuda):
     assert torch.all(claims == 1)
     assert torch.isfinite(loss).all() and torch.isfinite(w).all()
     assert not torch.equal(w.cpu(), torch.from_numpy(p))
+
+
+def test_train_session_equals_manual_epochs(chaos, torch_cuda):
+    """The per-epoch driver (Training, Validation on the training set, Testing)
+    equals the same calls made one by one; sequential mode, lr decaying."""
+    torch = torch_cuda
+    x, y = wl.train_set(500)
+    xt, yt = wl.test_set(300)
+    xd, yd = _dev(torch, x, torch.float32), _dev(torch, y, torch.int32)
+    xtd, ytd = _dev(torch, xt, torch.float32), _dev(torch, yt, torch.int32)
+    lr0, decay, epochs = 1e-2, 0.9, 3
+    net, _, p = _net(chaos, "small")
+    stats = net.train_session(xd, yd, xtd, ytd, epochs, lr0, decay, mode=chaos.SEQUENTIAL)
+    w_session = net.get_params()
+    ref, _, _ = _net(chaos, "small")
+    lr0f, decayf = float(np.float32(lr0)), float(np.float32(decay))
+    rows = []
+    for e in range(epochs):
+        lr = float(np.float32(lr0f * decayf ** e))
+        loss = torch.empty(500, device="cuda")
+        ref.train_epoch(xd, yd, lr, mode=chaos.SEQUENTIAL, loss=loss)
+        w_train = int(ref.evaluate(xd, yd).item())
+        w_test = int(ref.evaluate(xtd, ytd).item())
+        tl = torch.empty(300, device="cuda")
+        ref.forward_backward(xtd, ytd, loss=tl)
+        rows.append((loss.double().mean().item(), w_train, w_test, tl.double().mean().item()))
+    torch.cuda.synchronize()
+    assert torch.equal(w_session, ref.get_params())
+    st = stats.cpu().numpy()
+    for e, (ml, wtr, wte, mt) in enumerate(rows):
+        assert abs(st[e, 0] - ml) <= 1e-6 * ml and abs(st[e, 3] - mt) <= 1e-6 * mt
+        assert (st[e, 1], st[e, 2]) == (wtr, wte)
+    assert st[-1, 0] < st[0, 0]  # training loss goes down over the epochs
