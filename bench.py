@@ -99,6 +99,40 @@ def cpu_baseline(layers, p0, x, y, budget_s=15.0):
                       f"per-sample SGD (fp64 oracle, one thread), {dt:.1f} s"}
 
 
+def worker_sweep(chaos, wl, torch):
+    """Training samples/s against the number of concurrent Hogwild workers
+    (atomic pushes, lr 1e-3), one timed epoch per point after one warm-up
+    epoch; small worker counts run on a prefix of the training set."""
+    x, y = wl.train_set(60000)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    out = {}
+    for name in ("small", "medium", "large"):
+        layers = wl.NETS[name]
+        net = chaos.Net(layers, wl.init_params(layers))
+        flops, _ = train_flops_per_sample(layers)
+        counts, p = [], 1
+        while p < net.worker_limit:
+            counts.append(p)
+            p *= 2
+        counts = sorted(set(counts + [net.max_workers, net.worker_limit]))
+        rows = []
+        for w in counts:
+            n = min(60000, max(2000, 500 * w))
+            for _ in range(2):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                net.train_epoch(xd[:n], yd[:n], 1e-3, mode=chaos.HOGWILD_ATOMIC, workers=w)
+                b.record()
+                torch.cuda.synchronize()
+            sps = n / (a.elapsed_time(b) / 1e3)
+            rows.append({"workers": w, "samples": n, "samples_per_s": sps,
+                         "tflops": sps * flops / 1e12,
+                         "kernel": "fused" if w <= net.max_workers else "one-wavefront generic"})
+        out[name] = {"max_workers": net.max_workers, "worker_limit": net.worker_limit,
+                     "train_flop_per_sample": flops, "points": rows}
+    return {"sweep": "Hogwild training throughput vs concurrent workers", "nets": out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -110,6 +144,10 @@ def main():
     ap.add_argument("--samples", type=int, default=60000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rows", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the benchmark line, print one JSON line with training "
+                         "throughput against the number of Hogwild workers for the small, "
+                         "medium and large nets")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (calibrates "
                          "the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -133,6 +171,9 @@ def main():
     from paper_1506_09067_amd import chaos, workloads as wl
 
     torch.cuda.set_device(0)
+    if args.sweep:
+        print(json.dumps(worker_sweep(chaos, wl, torch)), flush=True)
+        return
     layers = wl.NETS[args.net]
     p0 = wl.init_params(layers)
     x, y = wl.train_set(args.samples)

@@ -117,7 +117,10 @@ int chaos_apply_update(chaos_net *net, const float *grad_dev, float lr, hipStrea
  * Hogwild, III-A.2) with no synchronisation between workers (Arbitrary Order
  * of Synchronization, III-A.3).  workers: number of concurrent workers for
  * the Hogwild modes (0 = chaos_max_workers(net)); ignored by
- * CHAOS_SEQUENTIAL.  Values above chaos_max_workers() are CHAOS_EINVAL.
+ * CHAOS_SEQUENTIAL.  Up to chaos_max_workers() the net's own kernel runs;
+ * above it, up to chaos_worker_limit(), every worker is one 64-thread
+ * wavefront of the generic kernel (per-worker state in HBM, allocated on
+ * first use).  Larger values are CHAOS_EINVAL.
  * loss_dev [n] (optional): each sample's loss at the time it was processed. */
 int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_dev, int64_t n,
                       float lr, int32_t mode, int32_t workers, float *loss_dev,
@@ -148,8 +151,13 @@ int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t 
                         int64_t n_test, int32_t epochs, float lr0, float decay, int32_t mode,
                         int32_t workers, float *stats_dev, hipStream_t stream);
 
-/* Largest number of concurrent Hogwild workers the device keeps resident. */
+/* Concurrent Hogwild workers the net's own kernel keeps resident (the
+ * default worker count). */
 int32_t chaos_max_workers(const chaos_net *net);
+
+/* Largest accepted worker count: one-wavefront workers of the generic kernel,
+ * up to 32 per compute unit (>= chaos_max_workers). */
+int32_t chaos_worker_limit(const chaos_net *net);
 
 /* Debug aid: when claims_dev (int32 [n] of the next chaos_train_epoch) is not
  * NULL, every processed sample index i adds 1 to claims_dev[i]; NULL turns it

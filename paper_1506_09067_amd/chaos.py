@@ -61,6 +61,7 @@ def lib():
             "chaos_train_session": ([P, P, P, i64, P, P, i64, i32, f32, f32, i32, i32, P, P],
                                     ctypes.c_int),
             "chaos_max_workers": ([P], ctypes.c_int32),
+            "chaos_worker_limit": ([P], ctypes.c_int32),
             "chaos_set_claim_counter": ([P, P], ctypes.c_int),
             "chaos_last_error": ([], ctypes.c_char_p),
         }
@@ -138,6 +139,10 @@ class Net:
     @property
     def max_workers(self) -> int:
         return int(lib().chaos_max_workers(self._h))
+
+    @property
+    def worker_limit(self) -> int:
+        return int(lib().chaos_worker_limit(self._h))
 
     def get_params(self, out=None):
         if out is None:

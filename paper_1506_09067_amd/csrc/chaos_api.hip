@@ -28,6 +28,8 @@ struct chaos_net {
     int fb_workers = 0;           // rows of grad_part
     float *grad_part = nullptr;   // [fb_workers][n_params]
     int32_t *claims = nullptr;    // debug claim counter (caller-owned)
+    int worker_limit = 0;         // one-wavefront generic workers the device keeps resident
+    float *wide_scratch = nullptr;  // [worker_limit][scratch_floats], allocated on first use
     float *sess_loss = nullptr;   // session: per-sample losses (training, then test)
     int64_t sess_loss_n = 0;
     int32_t *sess_wrong = nullptr;
@@ -216,6 +218,7 @@ int chaos_create_net(int32_t in_h, int32_t in_w, const chaos_layer *layers, int3
                             : chaos::worker_blocks_per_cu(net->block);
     if (per_cu < 1) { delete net; return fail(CHAOS_EDEVICE, "occupancy query failed"); }
     net->max_workers = per_cu * cus;
+    net->worker_limit = std::max(net->max_workers, chaos::worker_blocks_per_cu(64) * cus);
     // the fused kernels keep every per-sample value in LDS: no scratch
     size_t scratch_bytes = (net->fused || net->cpcp)
                                ? 0
@@ -242,6 +245,7 @@ int chaos_destroy_net(chaos_net *net) {
     (void)hipFree(net->scratch);
     (void)hipFree(net->counter);
     (void)hipFree(net->grad_part);
+    (void)hipFree(net->wide_scratch);
     (void)hipFree(net->sess_loss);
     (void)hipFree(net->sess_wrong);
     delete net;
@@ -261,6 +265,11 @@ int32_t chaos_num_outputs(const chaos_net *net) {
 int32_t chaos_max_workers(const chaos_net *net) {
     if (int rc = check_net(net)) return rc;
     return net->max_workers;
+}
+
+int32_t chaos_worker_limit(const chaos_net *net) {
+    if (int rc = check_net(net)) return rc;
+    return net->worker_limit;
 }
 
 int chaos_get_params(const chaos_net *net, float *dst_dev, hipStream_t stream) {
@@ -304,10 +313,31 @@ int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_
     if (int rc = check_io(x_dev, labels_dev, n)) return rc;
     if (mode != CHAOS_SEQUENTIAL && mode != CHAOS_HOGWILD_ATOMIC && mode != CHAOS_HOGWILD_RACY)
         return fail(CHAOS_EINVAL, "unknown mode %d", mode);
-    if (workers < 0 || workers > net->max_workers)
-        return fail(CHAOS_EINVAL, "workers=%d outside [0,%d]", workers, net->max_workers);
+    if (workers < 0 || workers > net->worker_limit)
+        return fail(CHAOS_EINVAL, "workers=%d outside [0,%d]", workers, net->worker_limit);
     if (int rc = set_device(net)) return rc;
     if (n == 0) return ok();
+    if (mode != CHAOS_SEQUENTIAL && workers > net->max_workers) {
+        // more workers than the net's kernel keeps resident: every worker is one
+        // 64-thread wavefront of the generic kernel, with scratch in HBM
+        if (!net->wide_scratch) {
+            size_t bytes = (size_t)net->worker_limit * net->desc.scratch_floats * sizeof(float);
+            if (hipMalloc(&net->wide_scratch, bytes) != hipSuccess) {
+                net->wide_scratch = nullptr;
+                return fail(CHAOS_ENOMEM, "scratch for %d workers", net->worker_limit);
+            }
+        }
+        chaos::WorkArgs a = base_args(net, x_dev, labels_dev, n);
+        a.scratch = net->wide_scratch;
+        a.lr = lr;
+        a.loss = loss_dev;
+        a.claims = net->claims;
+        int kmode = mode == CHAOS_HOGWILD_RACY ? chaos::kTrainRacy : chaos::kTrainAtomic;
+        int grid = (int)std::min<int64_t>(workers, n);
+        HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 1, stream), "counter reset");
+        HIP_TRY(chaos::launch_worker(kmode, net->desc, a, grid, 64, stream), "train launch");
+        return ok();
+    }
     int grid = 1;
     int kmode = chaos::kTrainAtomic;
     if (mode != CHAOS_SEQUENTIAL) {
@@ -377,12 +407,13 @@ int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t 
     if (epochs > 0 && !stats_dev) return fail(CHAOS_EINVAL, "stats_dev is NULL");
     if (mode != CHAOS_SEQUENTIAL && mode != CHAOS_HOGWILD_ATOMIC && mode != CHAOS_HOGWILD_RACY)
         return fail(CHAOS_EINVAL, "unknown mode %d", mode);
-    if (workers < 0 || workers > net->max_workers)
-        return fail(CHAOS_EINVAL, "workers=%d outside [0,%d]", workers, net->max_workers);
+    if (workers < 0 || workers > net->worker_limit)
+        return fail(CHAOS_EINVAL, "workers=%d outside [0,%d]", workers, net->worker_limit);
     if (int rc = set_device(net)) return rc;
     const int64_t need = std::max<int64_t>(std::max(n_train, n_test), 1);
     if (need > net->sess_loss_n) {
-        (void)hipFree(net->sess_loss);
+        (void)hipFree(net->wide_scratch);
+    (void)hipFree(net->sess_loss);
         net->sess_loss = nullptr;
         net->sess_loss_n = 0;
         if (hipMalloc(&net->sess_loss, (size_t)need * sizeof(float)) != hipSuccess)

@@ -202,7 +202,8 @@ __global__ void __launch_bounds__(256) worker_kernel(Net net, WorkArgs a) {
             in = ws + ly.y_off;
         }
         const float *yout = in;
-        if (a.out && threadIdx.x < net.n_out) a.out[idx * net.n_out + threadIdx.x] = yout[threadIdx.x];
+        if (a.out)
+            for (int k = threadIdx.x; k < net.n_out; k += blockDim.x) a.out[idx * net.n_out + k] = yout[k];
 
         if (MODE == kEvaluate) {
             if (threadIdx.x == 0) {

@@ -238,7 +238,7 @@ def test_bad_arguments_are_rejected(chaos, torch_cuda):
         net.train_epoch(xd, yd, 1e-3, mode=7)
     assert e.value.code == chaos.EINVAL
     with pytest.raises(chaos.ChaosError) as e:
-        net.train_epoch(xd, yd, 1e-3, workers=net.max_workers + 1)
+        net.train_epoch(xd, yd, 1e-3, workers=net.worker_limit + 1)
     assert e.value.code == chaos.EINVAL
 
 
@@ -345,3 +345,31 @@ def test_train_session_equals_manual_epochs(chaos, torch_cuda):
         assert abs(st[e, 0] - ml) <= 1e-6 * ml and abs(st[e, 3] - mt) <= 1e-6 * mt
         assert (st[e, 1], st[e, 2]) == (wtr, wte)
     assert st[-1, 0] < st[0, 0]  # training loss goes down over the epochs
+
+
+@pytest.mark.parametrize("name", ["small", "large"])
+def test_one_wavefront_workers_beyond_the_fused_capacity(chaos, torch_cuda, name):
+    """Worker counts above chaos_max_workers run one-wavefront generic workers:
+    every sample is claimed once, lr = 0 leaves the weights unchanged and the
+    per-sample losses match the oracle, training stays finite."""
+    torch = torch_cuda
+    net, layers, p = _net(chaos, name)
+    wmax = net.worker_limit
+    assert wmax >= 32 * 256 // 4 and wmax > net.max_workers
+    n = 20000 if name == "small" else 4000
+    x, y = wl.train_set(n)
+    xd, yd = _dev(torch, x, torch.float32), _dev(torch, y, torch.int32)
+    claims = torch.zeros(n, dtype=torch.int32, device="cuda")
+    net.set_claim_counter(claims)
+    loss = torch.empty(n, device="cuda")
+    net.train_epoch(xd, yd, 0.0, mode=chaos.HOGWILD_ATOMIC, workers=wmax, loss=loss)
+    net.set_claim_counter(None)
+    torch.cuda.synchronize()
+    assert torch.all(claims == 1)
+    assert torch.equal(net.get_params().cpu(), torch.from_numpy(p))
+    ref = np.array([orc.forward_backward(layers, p, x[i], int(y[i]), grad=False)["loss"]
+                    for i in range(0, n, n // 8)])
+    assert_close(loss.cpu().numpy()[::n // 8], ref, what="losses at lr 0")
+    net.train_epoch(xd, yd, 1e-3, mode=chaos.HOGWILD_ATOMIC, workers=wmax)
+    torch.cuda.synchronize()
+    assert torch.isfinite(net.get_params()).all()
