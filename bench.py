@@ -13,8 +13,11 @@ Prints one JSON line.  Extra fields:
                 MI355X FP32 peak
   cpu_baseline  the CPU oracle (sequential per-sample SGD, one core) on a
                 bounded sample of the same workload
-  rows          throughput of the frozen-weight 16,384-sample batch gradient
-                and of the 10,000-sample test forward pass
+  rows          training throughput of the small and medium nets on the same
+                set (every resident worker, with the FP32-peak fraction and
+                the oracle's sequential rate on a short prefix), and the
+                throughput of the frozen-weight 16,384-sample batch gradient
+                and of the 10,000-sample test forward pass of the large net
 """
 from __future__ import annotations
 
@@ -97,6 +100,33 @@ def cpu_baseline(layers, p0, x, y, budget_s=15.0):
     return {"value": n / dt, "unit": "training samples/s", "cores": 1, "kind": "oracle",
             "sample": f"first {n} samples of the 60,000-sample training set, sequential "
                       f"per-sample SGD (fp64 oracle, one thread), {dt:.1f} s"}
+
+
+def train_row(chaos, wl, torch, name, xd, yd, x, y, steps, with_cpu):
+    """Training throughput of one net over the resident training set with
+    every resident worker (atomic pushes, lr 1e-3)."""
+    layers = wl.NETS[name]
+    p0 = wl.init_params(layers)
+    net = chaos.Net(layers, p0)
+    flops, _ = train_flops_per_sample(layers)
+    n = yd.numel()
+    net.train_epoch(xd, yd, 1e-3, mode=chaos.HOGWILD_ATOMIC)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        net.train_epoch(xd, yd, 1e-3, mode=chaos.HOGWILD_ATOMIC)
+    b.record(stream)
+    torch.cuda.synchronize()
+    sps = n * steps / (a.elapsed_time(b) / 1e3)
+    tflops = sps * flops / 1e12
+    row = {"samples_per_s": sps, "workers": net.max_workers, "train_flop_per_sample": flops,
+           "tflops": tflops, "frac_fp32_peak": tflops / PEAK_FP32_TFLOPS,
+           "ms_per_epoch": a.elapsed_time(b) / steps}
+    if with_cpu:
+        row["cpu_oracle"] = cpu_baseline(layers, p0, x, y, budget_s=3.0)
+    return row
 
 
 def worker_sweep(chaos, wl, torch):
@@ -214,6 +244,11 @@ def main():
     rows = None
     if not args.no_rows:
         rows = {}
+        for name in ("small", "medium"):
+            if name != args.net:
+                rows[f"train_{name}_{args.samples}"] = train_row(
+                    chaos, wl, torch, name, xd, yd, x, y, args.steps,
+                    not args.no_cpu_baseline)
         xb, yb = wl.batch_set(16384)
         xbd, ybd = torch.from_numpy(xb).cuda(), torch.from_numpy(yb).cuda()
         g = torch.empty(net.n_params, device="cuda")
