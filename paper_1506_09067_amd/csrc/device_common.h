@@ -59,6 +59,24 @@ struct Push {
     }
 };
 
+// Orders the LDS accesses of this wavefront's lanes around this point (a
+// read after a write to the same word by another lane of the wavefront sees
+// the write).  The LDS serves one wavefront's instructions in issue order, so
+// it is enough that the compiler keeps them in program order; unlike a
+// workgroup fence this does not wait for outstanding global operations such
+// as weight pushes.
+__device__ __forceinline__ void wave_lds_order() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+}
+
+// Workgroup barrier that orders LDS only: the wavefronts' outstanding global
+// memory operations (weight pushes) stay in flight across it.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f4 mfma(float a, float b, f4 c) {

@@ -66,8 +66,8 @@ struct alignas(16) Smem {
         float red3[2 * 21 * 256];        // conv3 split-K partial sums (forward only)
         float w2s[KC2 * 65];             // conv2 weights staged as [k][o] (forward only)
     };
-    float p3[NF1];                       // pool2 output (FC1 input)
-    float e3[NF1];                       // dE/d(pool2 output)
+    alignas(16) float p3[NF1];           // pool2 output (FC1 input)
+    alignas(16) float e3[NF1];           // dE/d(pool2 output)
     float h[F1 + 10], dh[F1 + 10];
     float o[16], dout[16];
     float pushbuf[NW][16 * 65];          // per-wavefront transpose of a 16 x 64 gradient block
@@ -322,29 +322,62 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         }
         __syncthreads();
 
-        // FC1: four neurons per wavefront at a time, lanes across the 900
-        // inputs; all 60 weight loads of a round are issued before the sums
-        for (int j0 = 4 * wave; j0 < F1; j0 += 4 * NW) {
-            float wv[4][15];
+        // FC1: wavefront w computes neurons [38w, 38w + 38), eight at a time.
+        // Lane l holds inputs 4l + 256c (c < 4) and reads four consecutive
+        // weights of a row with one 16-byte load; the next eight rows are
+        // requested before the current ones are reduced.  The eight partial
+        // sums of a lane are reduced by halving: after exchanges with lanes
+        // l^32, l^16 and l^8 each lane keeps one neuron, and l^4, l^2, l^1
+        // complete its sum.
+        {
+            f4 xin[4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int it = 0; it < 15; ++it) {
-                    int j = j0 + q, i = lane + 64 * it;
-                    wv[q][it] = (j < F1 && i < NF1) ? W[OF1 + j * NF1 + i] : 0.0f;
-                }
-            float s[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int it = 0; it < 15; ++it) {
-                int i = lane + 64 * it;
-                float xi = (i < NF1) ? sm.p3[i] : 0.0f;
-#pragma unroll
-                for (int q = 0; q < 4; ++q) s[q] = fmaf(wv[q][it], xi, s[q]);
+            for (int c = 0; c < 4; ++c) {
+                int i = 4 * lane + 256 * c;
+                xin[c] = (i < NF1) ? *(const f4 *)(sm.p3 + i) : f4{0.f, 0.f, 0.f, 0.f};
             }
+            const int jb = 38 * wave, je = (jb + 38 < F1) ? jb + 38 : F1;
+            f4 wv[8][4];
+            auto load_rows = [&](int j0) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                float t = wave_sum(s[q]);
-                if (lane == 0 && j0 + q < F1) sm.h[j0 + q] = act_y(t + W[OBF1 + j0 + q]);
+                for (int q = 0; q < 8; ++q)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        int j = j0 + q, i = 4 * lane + 256 * c;
+                        wv[q][c] = (j < je && i < NF1) ? *(const f4 *)(W + OF1 + j * NF1 + i)
+                                                       : f4{0.f, 0.f, 0.f, 0.f};
+                    }
+            };
+            const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+            load_rows(jb);
+            for (int j0 = jb; j0 < je; j0 += 8) {
+                float sq[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    float t = 0.0f;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        t = fmaf(wv[q][c].x, xin[c].x, t);
+                        t = fmaf(wv[q][c].y, xin[c].y, t);
+                        t = fmaf(wv[q][c].z, xin[c].z, t);
+                        t = fmaf(wv[q][c].w, xin[c].w, t);
+                    }
+                    sq[q] = t;
+                }
+                if (j0 + 8 < je) load_rows(j0 + 8);
+                float t4[4], t2[2];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    t4[q] = (b5 ? sq[q + 4] : sq[q]) + __shfl_xor(b5 ? sq[q] : sq[q + 4], 32, 64);
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+                    t2[q] = (b4 ? t4[q + 2] : t4[q]) + __shfl_xor(b4 ? t4[q] : t4[q + 2], 16, 64);
+                float t1 = (b3 ? t2[1] : t2[0]) + __shfl_xor(b3 ? t2[0] : t2[1], 8, 64);
+                t1 += __shfl_xor(t1, 4, 64);
+                t1 += __shfl_xor(t1, 2, 64);
+                t1 += __shfl_xor(t1, 1, 64);
+                const int j = j0 + ((lane >> 3) & 7);
+                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[OBF1 + j]);
             }
         }
         __syncthreads();
@@ -406,42 +439,63 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             sm.dh[tid] = s * dact_from_y(sm.h[tid]);
         }
         __syncthreads();
-        // FC2 push; FC1 backward data (pre-update weights): thread per input,
-        // weights loaded 10 neurons at a time for 4 inputs per thread
+        // FC2 push; FC1 backward data (pre-update weights): thread t < 225
+        // owns inputs 4t..4t+3 and reads them from a row with one 16-byte
+        // load, ten rows per batch, the next batch requested before this one
+        // is summed (sum over rows in row order)
         for (int t = tid; t < F2 * F1; t += NT) {
             int j = t / F1, i = t - j * F1;
             push(OF2 + t, sm.dout[j] * sm.h[i]);
         }
         if (tid < F2) push(OBF2 + tid, sm.dout[tid]);
-        {
-            float s[4] = {0.f, 0.f, 0.f, 0.f};
-            for (int j0 = 0; j0 < F1; j0 += 10) {
-                float wv[4][10];
+        if (tid < NF1 / 4) {
+            f4 acc = {0.f, 0.f, 0.f, 0.f};
+            f4 wa[10], wb[10];
+            auto load = [&](f4 (&w)[10], int j0) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
-#pragma unroll
-                    for (int jj = 0; jj < 10; ++jj) {
-                        int i = tid + NT * q;
-                        wv[q][jj] = (i < NF1) ? W[OF1 + (j0 + jj) * NF1 + i] : 0.0f;
-                    }
+                for (int jj = 0; jj < 10; ++jj)
+                    w[jj] = *(const f4 *)(W + OF1 + (j0 + jj) * NF1 + 4 * tid);
+            };
+            auto comp = [&](const f4 (&w)[10], int j0) {
 #pragma unroll
                 for (int jj = 0; jj < 10; ++jj) {
                     float d = sm.dh[j0 + jj];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) s[q] = fmaf(wv[q][jj], d, s[q]);
+                    acc.x = fmaf(w[jj].x, d, acc.x);
+                    acc.y = fmaf(w[jj].y, d, acc.y);
+                    acc.z = fmaf(w[jj].z, d, acc.z);
+                    acc.w = fmaf(w[jj].w, d, acc.w);
+                }
+            };
+            load(wa, 0);
+            for (int j0 = 0; j0 < F1; j0 += 20) {
+                if (j0 + 10 < F1) load(wb, j0 + 10);
+                comp(wa, j0);
+                if (j0 + 10 < F1) {
+                    if (j0 + 20 < F1) load(wa, j0 + 20);
+                    comp(wb, j0 + 10);
                 }
             }
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                int i = tid + NT * q;
-                if (i < NF1) sm.e3[i] = s[q];
-            }
+            *(f4 *)(sm.e3 + 4 * tid) = acc;
         }
         __syncthreads();
         // FC1 push; pool2 backward -> conv3 output deltas d3[o][4P + w]; clear s2
-        for (int t = tid; t < F1 * NF1; t += NT) {
-            int j = t / NF1, i = t - j * NF1;
-            push(OF1 + t, sm.dh[j] * sm.p3[i]);
+        // (wavefront w pushes rows j = w, w + 4, ...; lane l the inputs
+        // l + 64c, so a push instruction covers 64 consecutive weights)
+        {
+            float xv[15];
+#pragma unroll
+            for (int c = 0; c < 15; ++c) {
+                int i = lane + 64 * c;
+                xv[c] = (i < NF1) ? sm.p3[i] : 0.0f;
+            }
+            for (int j = wave; j < F1; j += NW) {
+                const float d = sm.dh[j];
+#pragma unroll
+                for (int c = 0; c < 15; ++c) {
+                    int i = lane + 64 * c;
+                    if (i < NF1) push(OF1 + j * NF1 + i, d * xv[c]);
+                }
+            }
         }
         if (tid < F1) push(OBF1 + tid, sm.dh[tid]);
         for (int t = tid; t < C3 * M3P; t += NT) {
@@ -498,8 +552,8 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 }
             }
             // scatter grouped by kernel offset uv: inside a group the 3 x 64
-            // lanes write distinct addresses; the fence (an LDS wait) orders
-            // the groups, whose targets overlap
+            // lanes write distinct addresses; wave_lds_order() orders the
+            // groups, whose targets overlap
             float *dst = sm.s2 + (4 * blk + lg) * NY2;
             float *dm[3];
             bool mv[3];
@@ -517,7 +571,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                     for (int j = 0; j < 3; ++j)
                         if (mv[j]) dm[j][u * H2 + v] += acc[i][j][r];
-                    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+                    wave_lds_order();
                 }
         }
         __syncthreads();
@@ -563,14 +617,14 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     for (int t = 0; t < 4; ++t)
 #pragma unroll
                         for (int r = 0; r < 4; ++r) pb[(4 * lg + r) * 65 + 16 * t + lr] = acc[t][i][r];
-                    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+                    wave_lds_order();
 #pragma unroll
                     for (int row = 0; row < 16; ++row) {
                         int o = 16 * i + row;
                         float g = pb[row * 65 + lane];
                         if (o < C3 && kb < KC3) push(OW3 + o * KC3 + kb, g);
                     }
-                    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+                    wave_lds_order();
                 }
             }
             if (tid < C3) {
@@ -638,7 +692,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 }
             }
             // tiles 0..2: scatter grouped by kernel offset uv (distinct
-            // addresses inside a group, groups ordered by an LDS wait);
+            // addresses inside a group, groups kept in order);
             // tile 3 (one map, lanes at different uv may meet): LDS atomics
             float *e1 = sm.s2;
             float *dp[8];
@@ -659,7 +713,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                     for (int j = 0; j < 8; ++j)
                         if (pv[j]) dp[j][(c0 + lg) * NP1 + u * Q1 + v] += acc[i][j][r];
-                    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+                    wave_lds_order();
                 }
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
