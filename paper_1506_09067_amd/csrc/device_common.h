@@ -79,8 +79,18 @@ __device__ __forceinline__ void lds_barrier() {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
+// 16x16x4 fp32 MFMA: lane l supplies A[l%16][l/16] and B[l/16][l%16] and
+// holds C[4(l/16) + r][l%16] in element r.
 __device__ __forceinline__ f4 mfma(float a, float b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+typedef float f16 __attribute__((ext_vector_type(16)));
+
+// 32x32x2 fp32 MFMA: lane l supplies A[l%32][l/32] and B[l/32][l%32] and
+// holds C[8(r/4) + 4(l/32) + r%4][l%32] in element r.
+__device__ __forceinline__ f16 mfma32(float a, float b, f16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
 }
 
 // scaled tanh without its derivative (forward epilogues)

@@ -70,7 +70,7 @@ struct alignas(16) Smem {
     alignas(16) float e3[NF1];           // dE/d(pool2 output)
     float h[F1 + 10], dh[F1 + 10];
     float o[16], dout[16];
-    float pushbuf[NW][16 * 65];          // per-wavefront transpose of a 16 x 64 gradient block
+    alignas(16) float pushbuf[NW][16 * 65]; // per-wavefront transpose of a 16 x 64 gradient block
     alignas(16) int koff3[KC3];          // im2col offset into y2 of k = (c,u,v), conv3
     alignas(16) int koff2[KC2 + 4];      // im2col offset into p1 of k = (c,u,v), conv2
     unsigned char am1[C1 * NP1 + 12];    // pool1 argmax (window element 0..3)
@@ -141,28 +141,42 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             float b1[2];
 #pragma unroll
             for (int j = 0; j < 2; ++j) b1[j] = (16 * j + lr < C1) ? W[OB1 + 16 * j + lr] : 0.0f;
-            for (int i = wave; i < 43; i += NW) {
-                int m = 16 * i + lr, P = m >> 2;
-                bool valid = P < NP1;
-                int base = valid ? window_pos(P, m & 3, Q1, IN) : 0;
-                f4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
+            // a wavefront's tiles i = wave + 4q, six at a time (12 independent
+            // accumulators keep the matrix core busy)
+            for (int i0 = wave; i0 < 43; i0 += 6 * NW) {
+                f4 acc[6][2];
+                int base[6];
+                bool valid[6];
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    float av = valid ? sm.x[base + s * IN + lg] : 0.0f;
-                    acc0 = mfma(av, bw[s][0], acc0);
-                    acc1 = mfma(av, bw[s][1], acc1);
+                for (int q = 0; q < 6; ++q) {
+                    int m = 16 * (i0 + 4 * q) + lr, P = m >> 2;
+                    valid[q] = P < NP1;
+                    base[q] = valid[q] ? window_pos(P, m & 3, Q1, IN) : 0;
+                    acc[q][0] = f4{0.f, 0.f, 0.f, 0.f};
+                    acc[q][1] = acc[q][0];
                 }
-                int Pe = 4 * i + lg;
-                if (Pe < NP1) {
-                    float ym;
-                    int ag;
-                    pool4(acc0, b1[0], ym, ag);
-                    sm.p1[lr * NP1 + Pe] = ym;
-                    sm.am1[lr * NP1 + Pe] = (unsigned char)ag;
-                    if (16 + lr < C1) {
-                        pool4(acc1, b1[1], ym, ag);
-                        sm.p1[(16 + lr) * NP1 + Pe] = ym;
-                        sm.am1[(16 + lr) * NP1 + Pe] = (unsigned char)ag;
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+#pragma unroll
+                    for (int q = 0; q < 6; ++q) {
+                        float av = valid[q] ? sm.x[base[q] + s * IN + lg] : 0.0f;
+                        acc[q][0] = mfma(av, bw[s][0], acc[q][0]);
+                        acc[q][1] = mfma(av, bw[s][1], acc[q][1]);
+                    }
+#pragma unroll
+                for (int q = 0; q < 6; ++q) {
+                    int Pe = 4 * (i0 + 4 * q) + lg;
+                    if (Pe < NP1) {
+                        float ym;
+                        int ag;
+                        pool4(acc[q][0], b1[0], ym, ag);
+                        sm.p1[lr * NP1 + Pe] = ym;
+                        sm.am1[lr * NP1 + Pe] = (unsigned char)ag;
+                        if (16 + lr < C1) {
+                            pool4(acc[q][1], b1[1], ym, ag);
+                            sm.p1[(16 + lr) * NP1 + Pe] = ym;
+                            sm.am1[(16 + lr) * NP1 + Pe] = (unsigned char)ag;
+                        }
                     }
                 }
             }
@@ -516,8 +530,8 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         // same s2 entries.  Row q of tile i holds input map c0 + q/4 at kernel
         // offset uv = 4i + q%4: in the accumulator the four lane groups then
         // hold four different maps at one (u,v), so no scatter instruction
-        // has two lanes on one address.  The next output map's weights are
-        // loaded while the current one computes.
+        // has two lanes on one address.  The next output maps' weights and
+        // deltas are loaded while the current ones compute.
         for (int blk = wave; blk < C2 / 4; blk += NW) {
             f4 acc[9][3];
 #pragma unroll
@@ -526,34 +540,30 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 for (int j = 0; j < 3; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
             const int k0 = blk * 144;
             const int arow = k0 + (lr >> 2) * 36 + (lr & 3);
-            float aA[9], aB[9];
-            auto load_a = [&](float (&av)[9], int ks) {
+            float aA[9], aB[9], bA[3], bB[3];
+            auto load = [&](float (&av)[9], float (&bv)[3], int ks) {
                 const float *w3 = W + OW3 + (4 * ks + lg) * KC3 + arow;
 #pragma unroll
                 for (int i = 0; i < 9; ++i) av[i] = w3[4 * i];
-            };
-            auto compute = [&](const float (&av)[9], int ks) {
                 const float *dd = sm.d3 + (4 * ks + lg) * M3P + lr;
-                float bv[3];
 #pragma unroll
                 for (int j = 0; j < 3; ++j) bv[j] = dd[16 * j];
+            };
+            auto compute = [&](const float (&av)[9], const float (&bv)[3]) {
 #pragma unroll
                 for (int i = 0; i < 9; ++i)
 #pragma unroll
                     for (int j = 0; j < 3; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
             };
-            load_a(aA, 0);
+            load(aA, bA, 0);
             for (int ks = 0; ks < C3 / 4; ks += 2) {
-                if (ks + 1 < C3 / 4) load_a(aB, ks + 1);
-                compute(aA, ks);
+                if (ks + 1 < C3 / 4) load(aB, bB, ks + 1);
+                compute(aA, bA);
                 if (ks + 1 < C3 / 4) {
-                    if (ks + 2 < C3 / 4) load_a(aA, ks + 2);
-                    compute(aB, ks + 1);
+                    if (ks + 2 < C3 / 4) load(aA, bA, ks + 2);
+                    compute(aB, bB);
                 }
             }
-            // scatter grouped by kernel offset uv: inside a group the 3 x 64
-            // lanes write distinct addresses; wave_lds_order() orders the
-            // groups, whose targets overlap
             float *dst = sm.s2 + (4 * blk + lg) * NY2;
             float *dm[3];
             bool mv[3];
@@ -563,6 +573,9 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 mv[j] = m < M3;
                 dm[j] = dst + (mv[j] ? window_pos(m >> 2, m & 3, 3, H2) : 0);
             }
+            // scatter grouped by kernel offset uv: inside a group the 3 x 64
+            // lanes write distinct addresses; wave_lds_order() orders the
+            // groups, whose targets overlap
 #pragma unroll
             for (int i = 0; i < 9; ++i)
 #pragma unroll
@@ -576,61 +589,95 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         }
         __syncthreads();
 
-        // conv3 weight gradient: G[o][k] = sum_m d3[o][m] y2col[m][k], pushed
+        // conv3 weight gradient G[o][k] = sum_m d3[o][m] y2col[m][k], pushed.
+        // Maps 0..95 on 32x32x2 tiles: element r of a tile holds maps
+        // 8(r/4) + r%4 and that + 4 at 32 consecutive k, so a push
+        // instruction writes two 128-byte runs of weights.  Maps 96..99 on a
+        // 16x16x4 tile (rows 96..111), pushed by the lanes of rows 96..99,
+        // 16 consecutive k each.  Wavefront w takes the 64-column groups
+        // w, w + 4, ... (a column beyond KC3 computes values never pushed).
         {
-            float ad[7][9];
+            float a32[3][18];  // A[o = 32i + l%32][m = 2ms + l/32]
 #pragma unroll
-            for (int i = 0; i < 7; ++i)
+            for (int i = 0; i < 3; ++i)
 #pragma unroll
-                for (int s = 0; s < 9; ++s) {
-                    int o = 16 * i + lr;
-                    ad[i][s] = (o < C3) ? sm.d3[o * M3P + 4 * s + lg] : 0.0f;
-                }
-            // four adjacent column tiles (64 consecutive k) per step; each
-            // 16 x 64 block is transposed through LDS so that every push
-            // instruction covers 64 consecutive weights of one output map
-            // (256 contiguous bytes)
-            float *pb = sm.pushbuf[wave];
+                for (int ms = 0; ms < 18; ++ms)
+                    a32[i][ms] = sm.d3[(32 * i + (lane & 31)) * M3P + 2 * ms + (lane >> 5)];
+            float a16[9];      // A[o = 96 + l%16][m = 4s + l/16]
+#pragma unroll
+            for (int s9 = 0; s9 < 9; ++s9)
+                a16[s9] = (96 + lr < C3) ? sm.d3[(96 + lr) * M3P + 4 * s9 + lg] : 0.0f;
             for (int grp = wave; grp < (KC3 / 16 + 3) / 4; grp += NW) {
-                f4 acc[4][7];
+                f16 c32[3][2];
+                f4 c16[4];
 #pragma unroll
-                for (int t = 0; t < 4; ++t)
+                for (int i = 0; i < 3; ++i)
 #pragma unroll
-                    for (int i = 0; i < 7; ++i) acc[t][i] = f4{0.f, 0.f, 0.f, 0.f};
+                    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) c32[i][kt][r] = 0.0f;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) c16[t] = f4{0.f, 0.f, 0.f, 0.f};
+                const float *y32[2];
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+                    const int k = 64 * grp + 32 * kt + (lane & 31);
+                    y32[kt] = sm.y2 + (k < KC3 ? sm.koff3[k] : 0);
+                }
+                const float *y16[4];
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
                     const int k = 64 * grp + 16 * t + lr;
-                    if (64 * grp + 16 * t >= KC3) continue;
-                    const float *ycol = sm.y2 + sm.koff3[k];
+                    y16[t] = sm.y2 + (k < KC3 ? sm.koff3[k] : 0);
+                }
 #pragma unroll
-                    for (int s9 = 0; s9 < 9; ++s9) {
-                        int m = 4 * s9 + lg;
-                        float bv = ycol[window_pos(m >> 2, m & 3, 3, H2)];
+                for (int ms = 0; ms < 18; ++ms) {
+                    const int m = 2 * ms + (lane >> 5), wp = window_pos(m >> 2, m & 3, 3, H2);
+                    float bv[2];
 #pragma unroll
-                        for (int i = 0; i < 7; ++i) acc[t][i] = mfma(ad[i][s9], bv, acc[t][i]);
+                    for (int kt = 0; kt < 2; ++kt) bv[kt] = y32[kt][wp];
+#pragma unroll
+                    for (int i = 0; i < 3; ++i)
+#pragma unroll
+                        for (int kt = 0; kt < 2; ++kt) c32[i][kt] = mfma32(a32[i][ms], bv[kt], c32[i][kt]);
+                }
+#pragma unroll
+                for (int s9 = 0; s9 < 9; ++s9) {
+                    const int m = 4 * s9 + lg, wp = window_pos(m >> 2, m & 3, 3, H2);
+                    float bv[4];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) bv[t] = y16[t][wp];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) c16[t] = mfma(a16[s9], bv[t], c16[t]);
+                }
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+                    const int k = 64 * grp + 32 * kt + (lane & 31);
+                    if (k < KC3) {
+#pragma unroll
+                        for (int i = 0; i < 3; ++i)
+#pragma unroll
+                            for (int r = 0; r < 16; ++r) {
+                                const int o = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                                push(OW3 + o * KC3 + k, c32[i][kt][r]);
+                            }
                     }
                 }
-                const int kb = 64 * grp + lane;
 #pragma unroll
-                for (int i = 0; i < 7; ++i) {
+                for (int t = 0; t < 4; ++t) {
+                    const int k = 64 * grp + 16 * t + lr;
+                    if (lg == 0 && k < KC3) {
 #pragma unroll
-                    for (int t = 0; t < 4; ++t)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) pb[(4 * lg + r) * 65 + 16 * t + lr] = acc[t][i][r];
-                    wave_lds_order();
-#pragma unroll
-                    for (int row = 0; row < 16; ++row) {
-                        int o = 16 * i + row;
-                        float g = pb[row * 65 + lane];
-                        if (o < C3 && kb < KC3) push(OW3 + o * KC3 + kb, g);
+                        for (int r = 0; r < 4; ++r) push(OW3 + (96 + r) * KC3 + k, c16[t][r]);
                     }
-                    wave_lds_order();
                 }
             }
             if (tid < C3) {
-                float g = 0.0f;
-                for (int m = 0; m < M3; ++m) g += sm.d3[tid * M3P + m];
-                push(OB3 + tid, g);
+                // four partial sums over the window elements, then combined
+                float g4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int m = 0; m < M3; ++m) g4[m & 3] += sm.d3[tid * M3P + m];
+                push(OB3 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
             }
         }
         __syncthreads();
@@ -692,8 +739,8 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 }
             }
             // tiles 0..2: scatter grouped by kernel offset uv (distinct
-            // addresses inside a group, groups kept in order);
-            // tile 3 (one map, lanes at different uv may meet): LDS atomics
+            // addresses inside a group, groups kept in order); tile 3 (one
+            // map, lanes at different uv may meet): LDS atomics
             float *e1 = sm.s2;
             float *dp[8];
             bool pv[8];
@@ -777,33 +824,64 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     }
             }
             if (tid < C2) {
-                float g = 0.0f;
-                for (int p = 0; p < NY2; ++p) g += sm.y2[tid * NY2 + p];
-                push(OB2 + tid, g);
+                float g4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+                for (int p = 0; p < NY2; ++p) g4[p & 3] += sm.y2[tid * NY2 + p];
+                push(OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
             }
             for (int t = tid; t < C1 * NP1; t += NT) sm.s2[t] *= dact_from_y(sm.p1[t]);
         }
         __syncthreads();
 
-        // conv1 weight gradient from the pool1 deltas at each window's maximum
-        for (int t = tid; t < C1 * 16 + C1; t += NT) {
-            float g = 0.0f;
-            if (t < C1 * 16) {
-                int o = t >> 4, u = (t >> 2) & 3, v = t & 3;
-                const float *d1 = sm.s2 + o * NP1;
-                const unsigned char *am = sm.am1 + o * NP1;
-                const float *xs = sm.x + u * IN + v;
-                for (int py = 0; py < Q1; ++py)
+        // conv1 weight gradient G[o][uv] = sum over the 26x26 conv1 outputs
+        // of the delta (nonzero only at each pooling window's maximum) times
+        // the input under the kernel, as a GEMM on the matrix cores: rows o
+        // (2 tiles), cols uv = 4u + v, K = 4P + w with the pooled positions
+        // P split over the wavefronts; the four partial tiles are summed in
+        // wavefront order.  Bias gradient: the deltas summed per map.
+        {
+            f4 acc[2][2];
 #pragma unroll
-                    for (int px = 0; px < Q1; ++px) {
-                        int P = py * Q1 + px, w = am[P];
-                        g = fmaf(d1[P], xs[(2 * py + (w >> 1)) * IN + 2 * px + (w & 1)], g);
-                    }
-                push(OW1 + t, g);
-            } else {
-                int o = t - C1 * 16;
-                for (int P = 0; P < NP1; ++P) g += sm.s2[o * NP1 + P];
-                push(OB1 + o, g);
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int t = 0; t < 2; ++t) acc[h][t] = f4{0.f, 0.f, 0.f, 0.f};
+            const int oa = lr, ob = (16 + lr < C1) ? 16 + lr : 0;
+            const bool vb = 16 + lr < C1;
+            const int xo = ((lg >> 1) + (lr >> 2)) * IN + (lg & 1) + (lr & 3);
+            auto step = [&](int P, f4 (&c)[2]) {
+                const int py = P / Q1, px = P - py * Q1;
+                const float bx = sm.x[2 * py * IN + 2 * px + xo];
+                const float a0 = (sm.am1[oa * NP1 + P] == lg) ? sm.s2[oa * NP1 + P] : 0.0f;
+                const float a1 = (vb && sm.am1[ob * NP1 + P] == lg) ? sm.s2[ob * NP1 + P] : 0.0f;
+                c[0] = mfma(a0, bx, c[0]);
+                c[1] = mfma(a1, bx, c[1]);
+            };
+            int P = wave;
+            for (; P + NW < NP1; P += 2 * NW) {
+                step(P, acc[0]);
+                step(P + NW, acc[1]);
+            }
+            if (P < NP1) step(P, acc[0]);
+            float *red = sm.pushbuf[0];  // [wavefront][tile][lane][4]
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+                *(f4 *)(red + ((wave * 2 + t) * 64 + lane) * 4) = acc[0][t] + acc[1][t];
+            __syncthreads();
+            for (int t = tid; t < C1 * 16 + C1; t += NT) {
+                if (t < C1 * 16) {
+                    const int o = t >> 4, uv = t & 15, tile = o >> 4, row = o & 15;
+                    const int e = ((row >> 2) * 16 + uv) * 4 + (row & 3);
+                    float g = red[(0 * 2 + tile) * 256 + e];
+#pragma unroll
+                    for (int w = 1; w < NW; ++w) g += red[(w * 2 + tile) * 256 + e];
+                    push(OW1 + t, g);
+                } else {
+                    const int o = t - C1 * 16;
+                    float g4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+                    for (int q = 0; q < NP1; ++q) g4[q & 3] += sm.s2[o * NP1 + q];
+                    push(OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                }
             }
         }
         __syncthreads();
