@@ -85,6 +85,12 @@ __device__ __forceinline__ f4 mfma(float a, float b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// 4x4x1 fp32 MFMA, 16 blocks: lane l supplies A[l/4][l%4] and B[l/4][l%4]
+// of block l/4 and holds C[l/4][r][l%4] of that block in element r.
+__device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_4x4x1f32(a, b, c, 0, 0, 0);
+}
+
 typedef float f16 __attribute__((ext_vector_type(16)));
 
 // 32x32x2 fp32 MFMA: lane l supplies A[l%32][l/32] and B[l/32][l%32] and

@@ -592,10 +592,11 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         // conv3 weight gradient G[o][k] = sum_m d3[o][m] y2col[m][k], pushed.
         // Maps 0..95 on 32x32x2 tiles: element r of a tile holds maps
         // 8(r/4) + r%4 and that + 4 at 32 consecutive k, so a push
-        // instruction writes two 128-byte runs of weights.  Maps 96..99 on a
-        // 16x16x4 tile (rows 96..111), pushed by the lanes of rows 96..99,
-        // 16 consecutive k each.  Wavefront w takes the 64-column groups
-        // w, w + 4, ... (a column beyond KC3 computes values never pushed).
+        // instruction writes two 128-byte runs of weights.  Maps 96..99 on
+        // the 16-block 4x4x1 instruction with block b, column c at
+        // k = 4b + c: element r holds map 96 + r at 64 consecutive k.
+        // Wavefront w takes the 64-column groups w, w + 4, ... (a column
+        // beyond KC3 computes values never pushed).
         {
             float a32[3][18];  // A[o = 32i + l%32][m = 2ms + l/32]
 #pragma unroll
@@ -603,33 +604,18 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                 for (int ms = 0; ms < 18; ++ms)
                     a32[i][ms] = sm.d3[(32 * i + (lane & 31)) * M3P + 2 * ms + (lane >> 5)];
-            float a16[9];      // A[o = 96 + l%16][m = 4s + l/16]
-#pragma unroll
-            for (int s9 = 0; s9 < 9; ++s9)
-                a16[s9] = (96 + lr < C3) ? sm.d3[(96 + lr) * M3P + 4 * s9 + lg] : 0.0f;
+            const float *a4 = sm.d3 + (96 + (lane & 3)) * M3P;  // A[block][l%4][m]: map 96 + l%4
             for (int grp = wave; grp < (KC3 / 16 + 3) / 4; grp += NW) {
                 f16 c32[3][2];
-                f4 c16[4];
-#pragma unroll
-                for (int i = 0; i < 3; ++i)
-#pragma unroll
-                    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-                        for (int r = 0; r < 16; ++r) c32[i][kt][r] = 0.0f;
-#pragma unroll
-                for (int t = 0; t < 4; ++t) c16[t] = f4{0.f, 0.f, 0.f, 0.f};
+                f4 c4[2];
                 const float *y32[2];
 #pragma unroll
                 for (int kt = 0; kt < 2; ++kt) {
                     const int k = 64 * grp + 32 * kt + (lane & 31);
                     y32[kt] = sm.y2 + (k < KC3 ? sm.koff3[k] : 0);
                 }
-                const float *y16[4];
-#pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const int k = 64 * grp + 16 * t + lr;
-                    y16[t] = sm.y2 + (k < KC3 ? sm.koff3[k] : 0);
-                }
+                const int k4 = 64 * grp + lane;
+                const float *y4 = sm.y2 + (k4 < KC3 ? sm.koff3[k4] : 0);
 #pragma unroll
                 for (int ms = 0; ms < 18; ++ms) {
                     const int m = 2 * ms + (lane >> 5), wp = window_pos(m >> 2, m & 3, 3, H2);
@@ -639,16 +625,14 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                     for (int i = 0; i < 3; ++i)
 #pragma unroll
-                        for (int kt = 0; kt < 2; ++kt) c32[i][kt] = mfma32(a32[i][ms], bv[kt], c32[i][kt]);
+                        for (int kt = 0; kt < 2; ++kt)
+                            c32[i][kt] = mfma32(a32[i][ms], bv[kt], ms == 0 ? f16{} : c32[i][kt]);
                 }
+                // two partial sums (even and odd m) keep the chain short
 #pragma unroll
-                for (int s9 = 0; s9 < 9; ++s9) {
-                    const int m = 4 * s9 + lg, wp = window_pos(m >> 2, m & 3, 3, H2);
-                    float bv[4];
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) bv[t] = y16[t][wp];
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) c16[t] = mfma(a16[s9], bv[t], c16[t]);
+                for (int m = 0; m < M3; ++m) {
+                    const float bv = y4[window_pos(m >> 2, m & 3, 3, H2)];
+                    c4[m & 1] = mfma4(a4[m], bv, m < 2 ? f4{} : c4[m & 1]);
                 }
 #pragma unroll
                 for (int kt = 0; kt < 2; ++kt) {
@@ -663,13 +647,9 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                             }
                     }
                 }
+                if (k4 < KC3) {
 #pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const int k = 64 * grp + 16 * t + lr;
-                    if (lg == 0 && k < KC3) {
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) push(OW3 + (96 + r) * KC3 + k, c16[t][r]);
-                    }
+                    for (int r = 0; r < 4; ++r) push(OW3 + (96 + r) * KC3 + k4, c4[0][r] + c4[1][r]);
                 }
             }
             if (tid < C3) {
