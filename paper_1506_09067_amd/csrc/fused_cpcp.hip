@@ -25,8 +25,11 @@ struct Cpcp {
     static constexpr int NP2 = 9;                       // pool2 output 3x3
     static constexpr int NF1 = C2 * NP2;                // FC1 inputs
     static constexpr int KC2 = C1 * 25;                 // conv2 K = (c,u,v)
+    static constexpr int OW2_ = C1 * 16 + C1;           // offset of the conv2 weights
     static constexpr int KC2P = (KC2 + 15) / 16 * 16;   // padded to whole tiles
-    static constexpr int KS2 = (KC2 + 3) / 4;           // conv2 forward k-steps
+    static constexpr int KQ2 = (KC2 + 31) / 32 * 8;     // conv2 forward K padded to 4 KQ2
+    // 16-byte loads of conv2 weight rows need 16-byte aligned row starts
+    static constexpr bool W2_ALIGNED16 = (OW2_ % 4 == 0) && (KC2 % 4 == 0);
     static constexpr int CT1 = (C1 + 15) / 16;          // conv1 col tiles
     static constexpr int CT2 = (C2 + 15) / 16;          // conv2 map tiles
     static constexpr int C2P = CT2 * 16;
@@ -37,6 +40,8 @@ struct Cpcp {
     static constexpr int OF1 = OB2 + C2, OBF1 = OF1 + F1 * NF1;
     static constexpr int OF2 = OBF1 + F1, OBF2 = OF2 + F2 * F1;
     static constexpr int NPARAM = OBF2 + F2;
+    // FC1 rows read with 16-byte loads when every row start is 16-byte aligned
+    static constexpr int FC1_VEC = (OF1 % 4 == 0 && NF1 % 4 == 0) ? 4 : 1;
 };
 
 constexpr int NT = 256, NW = 4;
@@ -48,11 +53,13 @@ struct alignas(16) SmemCpcp {
     float p1[S::C1 * S::NP1];            // pool1 output, later pool1 errors/deltas in e1
     float e1[S::C1 * S::NP1];            // dE/d(pool1 output)
     float y2[S::C2 * S::NY2];            // conv2 output
-    float d2[S::C2P * 96];               // conv2 output deltas (dense, zero off the argmax)
-    float p2[S::NF1], e2[S::NF1];        // pool2 output / its errors
+    alignas(16) float d2[S::C2P * 96];   // conv2 output deltas (dense, zero off the argmax);
+                                         // conv2 forward partial sums before that
+    alignas(16) float p2[S::NF1];        // pool2 output
+    float e2[S::NF1], e2b[S::NF1];       // its errors (two partial sums over FC1 rows)
     float h[S::F1 + 16], dh[S::F1 + 16];
     float o[16], dout[16];
-    alignas(16) int koff2[S::KC2P];      // im2col offset into p1 of k = (c,u,v)
+    alignas(16) int koff2[4 * S::KQ2];   // im2col offset into p1 of k = (c,u,v) (0 past KC2)
     unsigned char am1[S::C1 * S::NP1 + 16];
     unsigned char am2[S::NF1 + 16];
     int64_t idx;
@@ -64,7 +71,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
     const float *W = a.params;
     constexpr bool kTrain = (MODE == kTrainAtomic || MODE == kTrainRacy);
 
-    for (int k = threadIdx.x; k < S::KC2P; k += NT) {
+    for (int k = threadIdx.x; k < 4 * S::KQ2; k += NT) {
         int c = k / 25, uv = k - 25 * c, u = uv / 5, v = uv - 5 * u;
         sm.koff2[k] = (k < S::KC2) ? c * S::NP1 + u * S::Q1 + v : 0;
     }
@@ -131,47 +138,108 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         __syncthreads();
 
         // ---- conv2: rows p < 81 (6 tiles), cols o < C2, K = C1*25 ----
-        for (int i = wave; i < RT2; i += NW) {
-            f4 acc[S::CT2];
+        // K in blocks of 16: at sub-step e of block b lane group g holds
+        // k = 16b + 4g + e, so a lane's four weights of a block are
+        // consecutive and the four lane groups of a row cover 64 contiguous
+        // bytes.  Wavefront w takes row tiles 3(w%2)..3(w%2)+2 and half of
+        // the blocks (w/2); the halves are added in a fixed order through LDS
+        // (the delta buffer is free during the forward pass).  Weights are
+        // requested two blocks ahead.
+        {
+            constexpr int NB = S::KQ2 / 8;  // blocks per half
+            const int rt0 = 3 * (wave & 1), half = wave >> 1;
+            f4 acc[3][S::CT2];
 #pragma unroll
-            for (int j = 0; j < S::CT2; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
-            int p = 16 * i + lr;
-            bool pv = p < S::NY2;
-            int py = p / S::H2, px = p - py * S::H2;
-            int base = pv ? py * S::Q1 + px : 0;
-            float bA[S::CT2], bB[S::CT2];
-            auto load_b = [&](float (&b)[S::CT2], int ks) {
-                int k = 4 * ks + lg;
+            for (int i = 0; i < 3; ++i)
 #pragma unroll
-                for (int j = 0; j < S::CT2; ++j) {
-                    int o = 16 * j + lr;
-                    b[j] = (o < S::C2 && k < S::KC2) ? W[S::OW2 + o * S::KC2 + k] : 0.0f;
-                }
-            };
-            auto compute = [&](const float (&b)[S::CT2], int ks) {
-                int k = 4 * ks + lg;
-                float av = (pv && k < S::KC2) ? sm.p1[base + sm.koff2[k]] : 0.0f;
+                for (int j = 0; j < S::CT2; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+            int base[3];
+            bool pv[3];
 #pragma unroll
-                for (int j = 0; j < S::CT2; ++j) acc[j] = mfma(av, b[j], acc[j]);
-            };
-            load_b(bA, 0);
-            for (int ks = 0; ks < S::KS2; ks += 2) {
-                if (ks + 1 < S::KS2) load_b(bB, ks + 1);
-                compute(bA, ks);
-                if (ks + 1 < S::KS2) {
-                    if (ks + 2 < S::KS2) load_b(bA, ks + 2);
-                    compute(bB, ks + 1);
-                }
+            for (int i = 0; i < 3; ++i) {
+                int p = 16 * (rt0 + i) + lr;
+                pv[i] = p < S::NY2;
+                int py = p / S::H2, px = p - py * S::H2;
+                base[i] = pv[i] ? py * S::Q1 + px : 0;
             }
+            const int kb = 16 * NB * half + 4 * lg;  // this lane's first k
+            const float *wrow[S::CT2];
+            bool ov[S::CT2];
 #pragma unroll
             for (int j = 0; j < S::CT2; ++j) {
                 int o = 16 * j + lr;
-                if (o >= S::C2) continue;
-                float bias = W[S::OB2 + o];
+                ov[j] = o < S::C2;
+                wrow[j] = W + S::OW2 + (ov[j] ? o : 0) * S::KC2 + kb;
+            }
+            float bw[3][S::CT2][4];
+            auto load = [&](float (&b)[S::CT2][4], int blk) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    int pe = 16 * i + 4 * lg + r;
-                    if (pe < S::NY2) sm.y2[o * S::NY2 + pe] = act_y(acc[j][r] + bias);
+                for (int j = 0; j < S::CT2; ++j) {
+                    if (S::W2_ALIGNED16) {
+                        f4 v = (ov[j] && kb + 16 * blk < S::KC2) ? *(const f4 *)(wrow[j] + 16 * blk)
+                                                                : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) b[j][e] = v[e];
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            int k = kb + 16 * blk + e;
+                            b[j][e] = (ov[j] && k < S::KC2) ? wrow[j][16 * blk + e] : 0.0f;
+                        }
+                    }
+                }
+            };
+            auto compute = [&](const float (&b)[S::CT2][4], int blk) {
+                const int4 ko = *(const int4 *)(sm.koff2 + kb + 16 * blk);
+                const int offs[4] = {ko.x, ko.y, ko.z, ko.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+#pragma unroll
+                    for (int i = 0; i < 3; ++i) {
+                        float av = pv[i] ? sm.p1[base[i] + offs[e]] : 0.0f;
+#pragma unroll
+                        for (int j = 0; j < S::CT2; ++j) acc[i][j] = mfma(av, b[j][e], acc[i][j]);
+                    }
+                }
+            };
+            load(bw[0], 0);
+            if (NB > 1) load(bw[1], 1);
+            for (int blk = 0; blk < NB; blk += 3) {
+                if (blk + 2 < NB) load(bw[2], blk + 2);
+                compute(bw[0], blk);
+                if (blk + 1 < NB) {
+                    if (blk + 3 < NB) load(bw[0], blk + 3);
+                    compute(bw[1], blk + 1);
+                }
+                if (blk + 2 < NB) {
+                    if (blk + 4 < NB) load(bw[1], blk + 4);
+                    compute(bw[2], blk + 2);
+                }
+            }
+            float *red = sm.d2 + (wave & 1) * (3 * S::CT2 * 256);
+            if (half == 1) {
+#pragma unroll
+                for (int i = 0; i < 3; ++i)
+#pragma unroll
+                    for (int j = 0; j < S::CT2; ++j)
+                        *(f4 *)(red + ((i * S::CT2 + j) * 64 + lane) * 4) = acc[i][j];
+            }
+            __syncthreads();
+            if (half == 0) {
+#pragma unroll
+                for (int j = 0; j < S::CT2; ++j) {
+                    int o = 16 * j + lr;
+                    if (o >= S::C2) continue;
+                    float bias = W[S::OB2 + o];
+#pragma unroll
+                    for (int i = 0; i < 3; ++i) {
+                        f4 t = acc[i][j] + *(const f4 *)(red + ((i * S::CT2 + j) * 64 + lane) * 4);
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            int pe = 16 * (rt0 + i) + 4 * lg + r;
+                            if (pe < S::NY2) sm.y2[o * S::NY2 + pe] = act_y(t[r] + bias);
+                        }
+                    }
                 }
             }
         }
@@ -194,31 +262,69 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         }
         __syncthreads();
 
-        // ---- FC1 and FC2 (one wavefront per neuron, lanes over inputs) ----
+        // ---- FC1: wavefront w computes neurons [JW w, JW w + JW), eight at a
+        //      time, lanes over the inputs (16-byte loads when the rows are
+        //      16-byte aligned); the eight partial sums of a lane are reduced
+        //      by halving (exchanges with lanes l^32, l^16, l^8 leave one
+        //      neuron per lane, l^4, l^2, l^1 complete it).  The next eight
+        //      rows are requested before the current ones are reduced. ----
         {
-            constexpr int IT = (S::NF1 + 63) / 64;
-            for (int j0 = 4 * wave; j0 < S::F1; j0 += 4 * NW) {
-                float wv[4][IT];
+            constexpr int VEC = S::FC1_VEC, IC = (S::NF1 + 64 * VEC - 1) / (64 * VEC);
+            constexpr int JW = (S::F1 + NW - 1) / NW;
+            float xin[IC][VEC];
+#pragma unroll
+            for (int c = 0; c < IC; ++c)
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+                    int i = VEC * lane + 64 * VEC * c + e;
+                    xin[c][e] = (i < S::NF1) ? sm.p2[i] : 0.0f;
+                }
+            const int jb = JW * wave, je = (jb + JW < S::F1) ? jb + JW : S::F1;
+            float wv[8][IC][VEC];
+            auto load_rows = [&](int j0) {
+#pragma unroll
+                for (int q = 0; q < 8; ++q)
+#pragma unroll
+                    for (int c = 0; c < IC; ++c) {
+                        const int j = j0 + q, i = VEC * lane + 64 * VEC * c;
+                        const bool v = j < je && i < S::NF1;
+                        const float *src = W + S::OF1 + (v ? j * S::NF1 + i : 0);
+                        if (VEC == 4) {
+                            f4 t = v ? *(const f4 *)src : f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) wv[q][c][e] = t[e];
+                        } else {
+                            wv[q][c][0] = v ? *src : 0.0f;
+                        }
+                    }
+            };
+            const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+            if (jb < je) load_rows(jb);
+            for (int j0 = jb; j0 < je; j0 += 8) {
+                float sq[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    float t = 0.0f;
+#pragma unroll
+                    for (int c = 0; c < IC; ++c)
+#pragma unroll
+                        for (int e = 0; e < VEC; ++e) t = fmaf(wv[q][c][e], xin[c][e], t);
+                    sq[q] = t;
+                }
+                if (j0 + 8 < je) load_rows(j0 + 8);
+                float t4[4], t2[2];
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
+                    t4[q] = (b5 ? sq[q + 4] : sq[q]) + __shfl_xor(b5 ? sq[q] : sq[q + 4], 32, 64);
 #pragma unroll
-                    for (int it = 0; it < IT; ++it) {
-                        int j = j0 + q, i = lane + 64 * it;
-                        wv[q][it] = (j < S::F1 && i < S::NF1) ? W[S::OF1 + j * S::NF1 + i] : 0.0f;
-                    }
-                float s[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int it = 0; it < IT; ++it) {
-                    int i = lane + 64 * it;
-                    float xi = (i < S::NF1) ? sm.p2[i] : 0.0f;
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) s[q] = fmaf(wv[q][it], xi, s[q]);
-                }
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    float t = wave_sum(s[q]);
-                    if (lane == 0 && j0 + q < S::F1) sm.h[j0 + q] = act_y(t + W[S::OBF1 + j0 + q]);
-                }
+                for (int q = 0; q < 2; ++q)
+                    t2[q] = (b4 ? t4[q + 2] : t4[q]) + __shfl_xor(b4 ? t4[q] : t4[q + 2], 16, 64);
+                float t1 = (b3 ? t2[1] : t2[0]) + __shfl_xor(b3 ? t2[0] : t2[1], 8, 64);
+                t1 += __shfl_xor(t1, 4, 64);
+                t1 += __shfl_xor(t1, 2, 64);
+                t1 += __shfl_xor(t1, 1, 64);
+                const int j = j0 + ((lane >> 3) & 7);
+                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[S::OBF1 + j]);
             }
         }
         __syncthreads();
@@ -283,24 +389,79 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             push(S::OF2 + t, sm.dout[j] * sm.h[i]);
         }
         if (tid < S::F2) push(S::OBF2 + tid, sm.dout[tid]);
-        for (int i = tid; i < S::NF1; i += NT) {
-            float s = 0.0f;
-            for (int j0 = 0; j0 < S::F1; j0 += 10) {
-                float wv[10];
+        // FC1 backward data (pre-update weights), summed over the rows in
+        // row order: thread t owns VEC inputs (one 16-byte load per row when
+        // aligned); with 16-byte loads the rows are split in two halves whose
+        // sums are added in the pool2 backward below.  Ten rows per batch,
+        // the next batch requested while this one is summed.
+        {
+            constexpr int VEC = S::FC1_VEC, NI = S::NF1 / VEC, NPART = (VEC == 4) ? 2 : 1;
+            constexpr int RP = (S::F1 + NPART - 1) / NPART;
+            if (tid < NI * NPART) {
+                const int i0 = VEC * (tid % NI), part = tid / NI;
+                const int r0 = part * RP, r1 = (r0 + RP < S::F1) ? r0 + RP : S::F1;
+                float acc[VEC];
 #pragma unroll
-                for (int jj = 0; jj < 10; ++jj)
-                    wv[jj] = (j0 + jj < S::F1) ? W[S::OF1 + (j0 + jj) * S::NF1 + i] : 0.0f;
+                for (int e = 0; e < VEC; ++e) acc[e] = 0.0f;
+                float wa[10][VEC], wb[10][VEC];
+                auto load = [&](float (&w)[10][VEC], int j0) {
 #pragma unroll
-                for (int jj = 0; jj < 10; ++jj)
-                    if (j0 + jj < S::F1) s = fmaf(wv[jj], sm.dh[j0 + jj], s);
+                    for (int jj = 0; jj < 10; ++jj) {
+                        const int j = j0 + jj;
+                        const float *src = W + S::OF1 + (j < r1 ? j : r0) * S::NF1 + i0;
+                        if (VEC == 4) {
+                            f4 t = *(const f4 *)src;
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) w[jj][e] = t[e];
+                        } else {
+                            w[jj][0] = *src;
+                        }
+                    }
+                };
+                auto comp = [&](const float (&w)[10][VEC], int j0) {
+#pragma unroll
+                    for (int jj = 0; jj < 10; ++jj) {
+                        if (j0 + jj < r1) {
+                            const float d = sm.dh[j0 + jj];
+#pragma unroll
+                            for (int e = 0; e < VEC; ++e) acc[e] = fmaf(w[jj][e], d, acc[e]);
+                        }
+                    }
+                };
+                load(wa, r0);
+                for (int j0 = r0; j0 < r1; j0 += 20) {
+                    if (j0 + 10 < r1) load(wb, j0 + 10);
+                    comp(wa, j0);
+                    if (j0 + 10 < r1) {
+                        if (j0 + 20 < r1) load(wa, j0 + 20);
+                        comp(wb, j0 + 10);
+                    }
+                }
+                float *dst = (part == 0) ? sm.e2 : sm.e2b;
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) dst[i0 + e] = acc[e];
             }
-            sm.e2[i] = s;
         }
         __syncthreads();
         // FC1 push; pool2 backward -> dense conv2 deltas; clear e1
-        for (int t = tid; t < S::F1 * S::NF1; t += NT) {
-            int j = t / S::NF1, i = t - j * S::NF1;
-            push(S::OF1 + t, sm.dh[j] * sm.p2[i]);
+        // (wavefront w pushes rows j = w, w + 4, ...; lane l the inputs
+        // l + 64c, so a push instruction covers up to 64 consecutive weights)
+        {
+            constexpr int IC = (S::NF1 + 63) / 64;
+            float xv[IC];
+#pragma unroll
+            for (int c = 0; c < IC; ++c) {
+                int i = lane + 64 * c;
+                xv[c] = (i < S::NF1) ? sm.p2[i] : 0.0f;
+            }
+            for (int j = wave; j < S::F1; j += NW) {
+                const float d = sm.dh[j];
+#pragma unroll
+                for (int c = 0; c < IC; ++c) {
+                    int i = lane + 64 * c;
+                    if (i < S::NF1) push(S::OF1 + j * S::NF1 + i, d * xv[c]);
+                }
+            }
         }
         if (tid < S::F1) push(S::OBF1 + tid, sm.dh[tid]);
         for (int t = tid; t < S::C2P * 96; t += NT) {
@@ -310,7 +471,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 int py = p / S::H2, px = p - py * S::H2;
                 int q = o * S::NP2 + (py / 3) * 3 + px / 3;
                 int w = (py % 3) * 3 + px % 3;
-                if (sm.am2[q] == w) d = sm.e2[q] * dact_from_y(sm.p2[q]);
+                if (sm.am2[q] == w) {
+                    const float e = (S::FC1_VEC == 4) ? sm.e2[q] + sm.e2b[q] : sm.e2[q];
+                    d = e * dact_from_y(sm.p2[q]);
+                }
             }
             sm.d2[t] = d;
         }
