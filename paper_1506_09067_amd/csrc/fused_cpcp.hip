@@ -85,11 +85,17 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 
         if (tid == 0) sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1)
                                       : (int64_t)blockIdx.x + step * gridDim.x;
+        // Reads are on demand: before any weight of this sample is read, one
+        // wavefront drops the weights this CU and its L2 hold from earlier
+        // samples (an agent-scope acquire: the caches are shared by the
+        // workgroup, and the barrier below orders every wavefront's reads
+        // after it).  The previous sample's barriers waited for all of this
+        // worker's pushes.
+        if (kTrain && wave == 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         __syncthreads();
         const int64_t idx = sm.idx;
         if (idx >= a.n) break;
         if (kTrain) {
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             if (a.claims && tid == 0) atomicAdd(a.claims + idx, 1);
         }
         const int label = a.labels[idx];
@@ -106,30 +112,44 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     int o = 16 * j + lr;
                     bw[s][j] = (o < S::C1) ? W[S::OW1 + o * 16 + 4 * s + lg] : 0.0f;
                 }
-            for (int i = wave; i < 43; i += NW) {
-                int m = 16 * i + lr, P = m >> 2;
-                bool valid = P < S::NP1;
-                int base = valid ? window_pos(P, m & 3, S::Q1, S::IN) : 0;
-                f4 acc[S::CT1];
+            float b1[S::CT1];
 #pragma unroll
-                for (int j = 0; j < S::CT1; ++j) acc[j] = f4{0.f, 0.f, 0.f, 0.f};
+            for (int j = 0; j < S::CT1; ++j) b1[j] = (16 * j + lr < S::C1) ? W[S::OB1 + 16 * j + lr] : 0.0f;
+            // a wavefront's tiles i = wave + 4q, six at a time
+            for (int i0 = wave; i0 < 43; i0 += 6 * NW) {
+                f4 acc[6][S::CT1];
+                int base[6];
+                bool valid[6];
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    float av = valid ? sm.x[base + s * S::IN + lg] : 0.0f;
+                for (int q = 0; q < 6; ++q) {
+                    int m = 16 * (i0 + 4 * q) + lr, P = m >> 2;
+                    valid[q] = P < S::NP1;
+                    base[q] = valid[q] ? window_pos(P, m & 3, S::Q1, S::IN) : 0;
 #pragma unroll
-                    for (int j = 0; j < S::CT1; ++j) acc[j] = mfma(av, bw[s][j], acc[j]);
+                    for (int j = 0; j < S::CT1; ++j) acc[q][j] = f4{0.f, 0.f, 0.f, 0.f};
                 }
-                int Pe = 4 * i + lg;
-                if (Pe < S::NP1) {
 #pragma unroll
-                    for (int j = 0; j < S::CT1; ++j) {
-                        int o = 16 * j + lr;
-                        if (o < S::C1) {
-                            float ym;
-                            int ag;
-                            pool4(acc[j], W[S::OB1 + o], ym, ag);
-                            sm.p1[o * S::NP1 + Pe] = ym;
-                            sm.am1[o * S::NP1 + Pe] = (unsigned char)ag;
+                for (int s = 0; s < 4; ++s)
+#pragma unroll
+                    for (int q = 0; q < 6; ++q) {
+                        float av = valid[q] ? sm.x[base[q] + s * S::IN + lg] : 0.0f;
+#pragma unroll
+                        for (int j = 0; j < S::CT1; ++j) acc[q][j] = mfma(av, bw[s][j], acc[q][j]);
+                    }
+#pragma unroll
+                for (int q = 0; q < 6; ++q) {
+                    int Pe = 4 * (i0 + 4 * q) + lg;
+                    if (Pe < S::NP1) {
+#pragma unroll
+                        for (int j = 0; j < S::CT1; ++j) {
+                            int o = 16 * j + lr;
+                            if (o < S::C1) {
+                                float ym;
+                                int ag;
+                                pool4(acc[q][j], b1[j], ym, ag);
+                                sm.p1[o * S::NP1 + Pe] = ym;
+                                sm.am1[o * S::NP1 + Pe] = (unsigned char)ag;
+                            }
                         }
                     }
                 }
@@ -482,48 +502,120 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         __syncthreads();
 
         // ---- conv2 backward data: C[(c,u,v)][p] = sum_o W2[o][c][u][v] d2[o][p],
-        //      col2im into e1[c][p + (u,v)].  Wavefront w owns input maps
-        //      c = w, w+4, ... (25 rows each, 2 tiles), so the LDS adds into a
-        //      map come from one wavefront in program order: reproducible. ----
-        for (int c = wave; c < S::C1; c += NW) {
-            f4 acc[2][RT2];
+        //      col2im into e1[c][p + (u,v)]. ----
+        if constexpr (S::C1 % 4 == 0) {
+            // Input maps in blocks of 4, a block owned by one wavefront.  Row
+            // q of tile i holds map c0 + q/4 at uv = 4i + q%4, so the four
+            // lane groups of an accumulator element hold four different maps
+            // at one (u,v): a scatter instruction never has two lanes on one
+            // address, and wave_lds_order() keeps the overlapping groups in
+            // order (plain read-add-write, no atomics).  Seven row tiles per
+            // block, computed in passes of four and three.
+            for (int blk = wave; blk < S::C1 / 4; blk += NW) {
+                const int c0 = 4 * blk;
 #pragma unroll
-            for (int t = 0; t < 2; ++t)
+                for (int pass = 0; pass < 2; ++pass) {
+                    constexpr int TI = 4;
+                    const int i0 = 4 * pass, nt = pass == 0 ? 4 : 3;
+                    f4 acc[TI][RT2];
 #pragma unroll
-                for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
-            for (int ks = 0; ks < S::OKS; ++ks) {
-                int o = 4 * ks + lg;
-                float av[2], bv[RT2];
+                    for (int t = 0; t < TI; ++t)
 #pragma unroll
-                for (int t = 0; t < 2; ++t) {
-                    int uv = 16 * t + lr;
-                    av[t] = (o < S::C2 && uv < 25) ? W[S::OW2 + o * S::KC2 + c * 25 + uv] : 0.0f;
-                }
+                        for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
+                    int wo[TI];  // offset of this lane's row in a weight row, or -1
 #pragma unroll
-                for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
-            }
-            float *ec = sm.e1 + c * S::NP1;
-#pragma unroll
-            for (int j = 0; j < RT2; ++j) {
-                int p = 16 * j + lr;
-                if (p >= S::NY2) continue;
-                int py = p / S::H2, px = p - py * S::H2;
-                float *ep = ec + py * S::Q1 + px;
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        int uv = 16 * t + 4 * lg + r;
-                        int u = uv / 5, v = uv - 5 * u;
-                        if (uv < 25)
-                            __hip_atomic_fetch_add(ep + u * S::Q1 + v, acc[t][j][r], __ATOMIC_RELAXED,
-                                                   __HIP_MEMORY_SCOPE_WORKGROUP);
+                    for (int t = 0; t < TI; ++t) {
+                        const int uv = 4 * (i0 + t) + (lr & 3);
+                        wo[t] = (t < nt && uv < 25) ? (c0 + (lr >> 2)) * 25 + uv : -1;
                     }
+                    // every k-step's weights requested at once (one memory
+                    // latency per pass)
+                    float av[S::OKS][TI];
+#pragma unroll
+                    for (int ks = 0; ks < S::OKS; ++ks) {
+                        const int o = 4 * ks + lg;
+                        const float *w2 = W + S::OW2 + (o < S::C2 ? o : 0) * S::KC2;
+#pragma unroll
+                        for (int t = 0; t < TI; ++t)
+                            av[ks][t] = (o < S::C2 && wo[t] >= 0) ? w2[wo[t]] : 0.0f;
+                    }
+#pragma unroll
+                    for (int ks = 0; ks < S::OKS; ++ks) {
+                        const int o = 4 * ks + lg;
+                        float bv[RT2];
+#pragma unroll
+                        for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
+#pragma unroll
+                        for (int t = 0; t < TI; ++t)
+#pragma unroll
+                            for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[ks][t], bv[j], acc[t][j]);
+                    }
+                    float *dp[RT2];
+                    bool pvv[RT2];
+#pragma unroll
+                    for (int j = 0; j < RT2; ++j) {
+                        const int p = 16 * j + lr;
+                        pvv[j] = p < S::NY2;
+                        const int py = p / S::H2, px = p - py * S::H2;
+                        dp[j] = sm.e1 + (c0 + lg) * S::NP1 + (pvv[j] ? py * S::Q1 + px : 0);
+                    }
+#pragma unroll
+                    for (int t = 0; t < TI; ++t)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            const int uv = 4 * (i0 + t) + r, u = uv / 5, v = uv - 5 * u;
+                            if (t >= nt || uv >= 25) continue;
+#pragma unroll
+                            for (int j = 0; j < RT2; ++j)
+                                if (pvv[j]) dp[j][u * S::Q1 + v] += acc[t][j][r];
+                            wave_lds_order();
+                        }
+                }
+            }
+        } else {
+            // Wavefront w owns input maps c = w, w+4, ... (25 rows each, 2
+            // tiles), so the LDS atomic adds into a map come from one
+            // wavefront in program order: reproducible.
+            for (int c = wave; c < S::C1; c += NW) {
+                f4 acc[2][RT2];
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+                for (int ks = 0; ks < S::OKS; ++ks) {
+                    int o = 4 * ks + lg;
+                    float av[2], bv[RT2];
+#pragma unroll
+                    for (int t = 0; t < 2; ++t) {
+                        int uv = 16 * t + lr;
+                        av[t] = (o < S::C2 && uv < 25) ? W[S::OW2 + o * S::KC2 + c * 25 + uv] : 0.0f;
+                    }
+#pragma unroll
+                    for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
+#pragma unroll
+                    for (int t = 0; t < 2; ++t)
+#pragma unroll
+                        for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
+                }
+                float *ec = sm.e1 + c * S::NP1;
+#pragma unroll
+                for (int j = 0; j < RT2; ++j) {
+                    int p = 16 * j + lr;
+                    if (p >= S::NY2) continue;
+                    int py = p / S::H2, px = p - py * S::H2;
+                    float *ep = ec + py * S::Q1 + px;
+#pragma unroll
+                    for (int t = 0; t < 2; ++t)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            int uv = 16 * t + 4 * lg + r;
+                            int u = uv / 5, v = uv - 5 * u;
+                            if (uv < 25)
+                                __hip_atomic_fetch_add(ep + u * S::Q1 + v, acc[t][j][r], __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_WORKGROUP);
+                        }
+                }
             }
         }
         __syncthreads();
@@ -543,59 +635,113 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 int py = p / S::H2, px = p - py * S::H2;
                 pb[s] = (p < S::NY2) ? py * S::Q1 + px : -1;
             }
-            for (int jt = wave; jt < S::KC2P / 16; jt += NW) {
-                int k = 16 * jt + lr;
-                bool kv = k < S::KC2;
-                const float *pc = sm.p1 + (kv ? sm.koff2[k] : 0);
-                f4 acc[S::CT2];
+            // JB column tiles of 16 k per pass, so that JB * CT2 accumulators
+            // keep the matrix core busy
+            constexpr int NJT = S::KC2P / 16, JB = (NJT / NW >= 4) ? 4 : 2;
+            static_assert(NJT % (NW * JB) == 0, "whole passes");
+            for (int jt0 = wave * JB; jt0 < NJT; jt0 += NW * JB) {
+                const float *pc[JB];
+                bool kv[JB];
 #pragma unroll
-                for (int i = 0; i < S::CT2; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+                for (int b = 0; b < JB; ++b) {
+                    const int k = 16 * (jt0 + b) + lr;
+                    kv[b] = k < S::KC2;
+                    pc[b] = sm.p1 + (kv[b] ? sm.koff2[k] : 0);
+                }
+                f4 acc[JB][S::CT2];
+#pragma unroll
+                for (int b = 0; b < JB; ++b)
+#pragma unroll
+                    for (int i = 0; i < S::CT2; ++i) acc[b][i] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int s = 0; s < 21; ++s) {
-                    float bv = (kv && pb[s] >= 0) ? pc[pb[s]] : 0.0f;
+                    float bv[JB];
 #pragma unroll
-                    for (int i = 0; i < S::CT2; ++i) acc[i] = mfma(ad[i][s], bv, acc[i]);
+                    for (int b = 0; b < JB; ++b) bv[b] = (kv[b] && pb[s] >= 0) ? pc[b][pb[s]] : 0.0f;
+#pragma unroll
+                    for (int b = 0; b < JB; ++b)
+#pragma unroll
+                        for (int i = 0; i < S::CT2; ++i) acc[b][i] = mfma(ad[i][s], bv[b], acc[b][i]);
                 }
-                if (kv) {
+#pragma unroll
+                for (int b = 0; b < JB; ++b) {
+                    if (!kv[b]) continue;
+                    const int k = 16 * (jt0 + b) + lr;
 #pragma unroll
                     for (int i = 0; i < S::CT2; ++i)
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             int o = 16 * i + 4 * lg + r;
-                            if (o < S::C2) push(S::OW2 + o * S::KC2 + k, acc[i][r]);
+                            if (o < S::C2) push(S::OW2 + o * S::KC2 + k, acc[b][i][r]);
                         }
                 }
             }
             if (tid < S::C2) {
-                float g = 0.0f;
-#pragma unroll 8
-                for (int p = 0; p < S::NY2; ++p) g += sm.d2[tid * 96 + p];
-                push(S::OB2 + tid, g);
+                float g4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+                for (int p = 0; p < S::NY2; ++p) g4[p & 3] += sm.d2[tid * 96 + p];
+                push(S::OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
             }
             for (int t = tid; t < S::C1 * S::NP1; t += NT) sm.e1[t] *= dact_from_y(sm.p1[t]);
         }
         __syncthreads();
 
-        // ---- conv1 weight gradient from the pool1 deltas at each window's maximum ----
-        for (int t = tid; t < S::C1 * 16 + S::C1; t += NT) {
-            float g = 0.0f;
-            if (t < S::C1 * 16) {
-                int o = t >> 4, u = (t >> 2) & 3, v = t & 3;
-                const float *d1 = sm.e1 + o * S::NP1;
-                const unsigned char *am = sm.am1 + o * S::NP1;
-                const float *xs = sm.x + u * S::IN + v;
-                for (int py = 0; py < S::Q1; ++py)
+        // ---- conv1 weight gradient G[o][uv] = sum over the 26x26 conv1 outputs
+        //      of the delta (nonzero only at each pooling window's maximum)
+        //      times the input under the kernel, on the matrix cores: rows o,
+        //      cols uv = 4u + v, K = 4P + w with the pooled positions P split
+        //      over the wavefronts; the partial tiles are summed in wavefront
+        //      order (through the free delta buffer).  Bias: deltas summed per
+        //      map. ----
+        {
+            f4 acc[2][S::CT1];
 #pragma unroll
-                    for (int px = 0; px < S::Q1; ++px) {
-                        int P = py * S::Q1 + px, w = am[P];
-                        g = fmaf(d1[P], xs[(2 * py + (w >> 1)) * S::IN + 2 * px + (w & 1)], g);
-                    }
-                push(S::OW1 + t, g);
-            } else {
-                int o = t - S::C1 * 16;
-#pragma unroll 8
-                for (int P = 0; P < S::NP1; ++P) g += sm.e1[o * S::NP1 + P];
-                push(S::OB1 + o, g);
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int t = 0; t < S::CT1; ++t) acc[h][t] = f4{0.f, 0.f, 0.f, 0.f};
+            int orow[S::CT1];
+            bool ov[S::CT1];
+#pragma unroll
+            for (int t = 0; t < S::CT1; ++t) {
+                ov[t] = 16 * t + lr < S::C1;
+                orow[t] = (ov[t] ? 16 * t + lr : 0) * S::NP1;
+            }
+            const int xo = ((lg >> 1) + (lr >> 2)) * S::IN + (lg & 1) + (lr & 3);
+            auto step = [&](int P, f4 (&c)[S::CT1]) {
+                const int py = P / S::Q1, px = P - py * S::Q1;
+                const float bx = sm.x[2 * py * S::IN + 2 * px + xo];
+#pragma unroll
+                for (int t = 0; t < S::CT1; ++t) {
+                    const float av = (ov[t] && sm.am1[orow[t] + P] == lg) ? sm.e1[orow[t] + P] : 0.0f;
+                    c[t] = mfma(av, bx, c[t]);
+                }
+            };
+            int P = wave;
+            for (; P + NW < S::NP1; P += 2 * NW) {
+                step(P, acc[0]);
+                step(P + NW, acc[1]);
+            }
+            if (P < S::NP1) step(P, acc[0]);
+            float *red = sm.d2;  // [wavefront][tile][lane][4]
+#pragma unroll
+            for (int t = 0; t < S::CT1; ++t)
+                *(f4 *)(red + ((wave * S::CT1 + t) * 64 + lane) * 4) = acc[0][t] + acc[1][t];
+            __syncthreads();
+            for (int t = tid; t < S::C1 * 16 + S::C1; t += NT) {
+                if (t < S::C1 * 16) {
+                    const int o = t >> 4, uv = t & 15, tile = o >> 4, row = o & 15;
+                    const int e = ((row >> 2) * 16 + uv) * 4 + (row & 3);
+                    float g = red[(0 * S::CT1 + tile) * 256 + e];
+#pragma unroll
+                    for (int w = 1; w < NW; ++w) g += red[(w * S::CT1 + tile) * 256 + e];
+                    push(S::OW1 + t, g);
+                } else {
+                    const int o = t - S::C1 * 16;
+                    float g4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+                    for (int q = 0; q < S::NP1; ++q) g4[q & 3] += sm.e1[o * S::NP1 + q];
+                    push(S::OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                }
             }
         }
         __syncthreads();
@@ -605,6 +751,8 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 using Small = Cpcp<5, 10, 50>;
 using Medium = Cpcp<20, 40, 150>;
 static_assert(Small::NPARAM == 6405 && Medium::NPARAM == 76040, "Table I weight counts");
+static_assert(NW * Small::CT1 * 256 <= Small::C2P * 96 && NW * Medium::CT1 * 256 <= Medium::C2P * 96,
+              "conv1 partial tiles fit in the delta buffer");
 
 template <class S, int MINB>
 hipError_t launch_cpcp(int mode, const WorkArgs &a, int grid, hipStream_t s) {
