@@ -57,6 +57,28 @@ struct Push {
                 __hip_atomic_fetch_add(part + off, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
+
+    // The same push, returning the weight it found: the value just before
+    // this push (training) or the unchanged weight (frozen).  A layer whose
+    // partial derivatives need its own weights can take them from here in
+    // one pass instead of reading them before pushing.
+    __device__ __forceinline__ float with_old(int off, float g) const {
+        if (mode == kTrainAtomic) {
+            return __hip_atomic_fetch_add(params + off, __fmul_rn(neg_lr, g), __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+        } else if (mode == kTrainRacy) {
+            float w = __hip_atomic_load(params + off, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(params + off, __fadd_rn(w, __fmul_rn(neg_lr, g)), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+            return w;
+        } else {
+            const float w = params[off];
+            if (each) each[off] = g;
+            if (part)
+                __hip_atomic_fetch_add(part + off, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return w;
+        }
+    }
 };
 
 // Orders the LDS accesses of this wavefront's lanes around this point (a

@@ -78,6 +78,7 @@ struct alignas(16) Smem {
     int64_t idx;
 };
 static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
+static_assert(NW * 16 * 65 >= NW * NF1, "FC1 partial sums fit in the transpose buffer");
 
 template <int MODE>
 __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
@@ -458,65 +459,116 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             sm.dh[tid] = s * dact_from_y(sm.h[tid]);
         }
         __syncthreads();
-        // FC2 push; FC1 backward data (pre-update weights): thread t < 225
-        // owns inputs 4t..4t+3 and reads them from a row with one 16-byte
-        // load, ten rows per batch, the next batch requested before this one
-        // is summed (sum over rows in row order)
+        // FC2 push.  FC1 push and FC1 backward data in one pass: each push
+        // returns the weight it updated, which is this layer's pre-update
+        // weight (Section III-A.2), so e3[i] = sum_j W[j][i] dh[j] needs no
+        // separate read of the 540 KB of FC1 weights.  Wavefront w pushes
+        // rows j = w, w + 4, ... (lane l the inputs l + 64c, a push
+        // instruction covers 64 consecutive weights) and keeps a partial sum
+        // per input; the four partial sums are added in wavefront order.
         for (int t = tid; t < F2 * F1; t += NT) {
             int j = t / F1, i = t - j * F1;
             push(OF2 + t, sm.dout[j] * sm.h[i]);
         }
         if (tid < F2) push(OBF2 + tid, sm.dout[tid]);
-        if (tid < NF1 / 4) {
-            f4 acc = {0.f, 0.f, 0.f, 0.f};
-            f4 wa[10], wb[10];
-            auto load = [&](f4 (&w)[10], int j0) {
+        if (tid < F1) push(OBF1 + tid, sm.dh[tid]);
+        if constexpr (MODE == kForwardBackward) {
+            // frozen weights: read them (16-byte loads, ten rows per batch,
+            // the next batch requested while this one is summed), then push
+            if (tid < NF1 / 4) {
+                f4 acc = {0.f, 0.f, 0.f, 0.f};
+                f4 wa[10], wb[10];
+                auto load = [&](f4 (&w)[10], int j0) {
 #pragma unroll
-                for (int jj = 0; jj < 10; ++jj)
-                    w[jj] = *(const f4 *)(W + OF1 + (j0 + jj) * NF1 + 4 * tid);
-            };
-            auto comp = [&](const f4 (&w)[10], int j0) {
+                    for (int jj = 0; jj < 10; ++jj)
+                        w[jj] = *(const f4 *)(W + OF1 + (j0 + jj) * NF1 + 4 * tid);
+                };
+                auto comp = [&](const f4 (&w)[10], int j0) {
 #pragma unroll
-                for (int jj = 0; jj < 10; ++jj) {
-                    float d = sm.dh[j0 + jj];
-                    acc.x = fmaf(w[jj].x, d, acc.x);
-                    acc.y = fmaf(w[jj].y, d, acc.y);
-                    acc.z = fmaf(w[jj].z, d, acc.z);
-                    acc.w = fmaf(w[jj].w, d, acc.w);
+                    for (int jj = 0; jj < 10; ++jj) {
+                        float d = sm.dh[j0 + jj];
+                        acc.x = fmaf(w[jj].x, d, acc.x);
+                        acc.y = fmaf(w[jj].y, d, acc.y);
+                        acc.z = fmaf(w[jj].z, d, acc.z);
+                        acc.w = fmaf(w[jj].w, d, acc.w);
+                    }
+                };
+                load(wa, 0);
+                for (int j0 = 0; j0 < F1; j0 += 20) {
+                    if (j0 + 10 < F1) load(wb, j0 + 10);
+                    comp(wa, j0);
+                    if (j0 + 10 < F1) {
+                        if (j0 + 20 < F1) load(wa, j0 + 20);
+                        comp(wb, j0 + 10);
+                    }
                 }
-            };
-            load(wa, 0);
-            for (int j0 = 0; j0 < F1; j0 += 20) {
-                if (j0 + 10 < F1) load(wb, j0 + 10);
-                comp(wa, j0);
-                if (j0 + 10 < F1) {
-                    if (j0 + 20 < F1) load(wa, j0 + 20);
-                    comp(wb, j0 + 10);
-                }
+                *(f4 *)(sm.e3 + 4 * tid) = acc;
             }
-            *(f4 *)(sm.e3 + 4 * tid) = acc;
-        }
-        __syncthreads();
-        // FC1 push; pool2 backward -> conv3 output deltas d3[o][4P + w]; clear s2
-        // (wavefront w pushes rows j = w, w + 4, ...; lane l the inputs
-        // l + 64c, so a push instruction covers 64 consecutive weights)
-        {
-            float xv[15];
-#pragma unroll
-            for (int c = 0; c < 15; ++c) {
-                int i = lane + 64 * c;
-                xv[c] = (i < NF1) ? sm.p3[i] : 0.0f;
-            }
-            for (int j = wave; j < F1; j += NW) {
-                const float d = sm.dh[j];
+            {
+                float xv[15];
 #pragma unroll
                 for (int c = 0; c < 15; ++c) {
                     int i = lane + 64 * c;
-                    if (i < NF1) push(OF1 + j * NF1 + i, d * xv[c]);
+                    xv[c] = (i < NF1) ? sm.p3[i] : 0.0f;
+                }
+                for (int j = wave; j < F1; j += NW) {
+                    const float d = sm.dh[j];
+#pragma unroll
+                    for (int c = 0; c < 15; ++c) {
+                        int i = lane + 64 * c;
+                        if (i < NF1) push(OF1 + j * NF1 + i, d * xv[c]);
+                    }
+                }
+            }
+        } else {
+            {
+                float xv[15], ep[15];
+#pragma unroll
+                for (int c = 0; c < 15; ++c) {
+                    int i = lane + 64 * c;
+                    xv[c] = (i < NF1) ? sm.p3[i] : 0.0f;
+                    ep[c] = 0.0f;
+                }
+                // two rows per step: 30 pushes in flight before their returns are used
+                for (int j = wave; j < F1; j += 2 * NW) {
+                    const int j2 = j + NW;
+                    const float d = sm.dh[j], d2 = (j2 < F1) ? sm.dh[j2] : 0.0f;
+                    float old[2][15];
+#pragma unroll
+                    for (int c = 0; c < 15; ++c) {
+                        int i = lane + 64 * c;
+                        old[0][c] = (i < NF1) ? push.with_old(OF1 + j * NF1 + i, d * xv[c]) : 0.0f;
+                    }
+                    if (j2 < F1) {
+#pragma unroll
+                        for (int c = 0; c < 15; ++c) {
+                            int i = lane + 64 * c;
+                            old[1][c] = (i < NF1) ? push.with_old(OF1 + j2 * NF1 + i, d2 * xv[c]) : 0.0f;
+                        }
+                    } else {
+#pragma unroll
+                        for (int c = 0; c < 15; ++c) old[1][c] = 0.0f;
+                    }
+#pragma unroll
+                    for (int c = 0; c < 15; ++c) ep[c] = fmaf(old[1][c], d2, fmaf(old[0][c], d, ep[c]));
+                }
+                float *part = sm.pushbuf[0];  // [wavefront][input]
+#pragma unroll
+                for (int c = 0; c < 15; ++c) {
+                    int i = lane + 64 * c;
+                    if (i < NF1) part[wave * NF1 + i] = ep[c];
                 }
             }
         }
-        if (tid < F1) push(OBF1 + tid, sm.dh[tid]);
+        __syncthreads();
+        // e3 = the partial sums in wavefront order (training); pool2
+        // backward -> conv3 output deltas d3[o][4P + w]; clear s2
+        if constexpr (MODE != kForwardBackward) {
+            const float *part = sm.pushbuf[0];
+            for (int q = tid; q < NF1; q += NT)
+                sm.e3[q] = ((part[q] + part[NF1 + q]) + part[2 * NF1 + q]) + part[3 * NF1 + q];
+            __syncthreads();
+        }
         for (int t = tid; t < C3 * M3P; t += NT) {
             int o = t / M3P, m = t - o * M3P;
             float d = 0.0f;
