@@ -403,87 +403,127 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             sm.dh[i] = s * dact_from_y(sm.h[i]);
         }
         __syncthreads();
-        // FC2 push; FC1 backward data (pre-update weights)
+        // FC2 push; FC1 push and FC1 backward data
         for (int t = tid; t < S::F2 * S::F1; t += NT) {
             int j = t / S::F1, i = t - j * S::F1;
             push(S::OF2 + t, sm.dout[j] * sm.h[i]);
         }
         if (tid < S::F2) push(S::OBF2 + tid, sm.dout[tid]);
-        // FC1 backward data (pre-update weights), summed over the rows in
-        // row order: thread t owns VEC inputs (one 16-byte load per row when
-        // aligned); with 16-byte loads the rows are split in two halves whose
-        // sums are added in the pool2 backward below.  Ten rows per batch,
-        // the next batch requested while this one is summed.
-        {
-            constexpr int VEC = S::FC1_VEC, NI = S::NF1 / VEC, NPART = (VEC == 4) ? 2 : 1;
-            constexpr int RP = (S::F1 + NPART - 1) / NPART;
-            if (tid < NI * NPART) {
-                const int i0 = VEC * (tid % NI), part = tid / NI;
-                const int r0 = part * RP, r1 = (r0 + RP < S::F1) ? r0 + RP : S::F1;
-                float acc[VEC];
+        if constexpr (MODE == kForwardBackward) {
+            // frozen weights: read them, then push
+            // FC1 backward data (pre-update weights), summed over the rows in
+            // row order: thread t owns VEC inputs (one 16-byte load per row when
+            // aligned); with 16-byte loads the rows are split in two halves whose
+            // sums are added in the pool2 backward below.  Ten rows per batch,
+            // the next batch requested while this one is summed.
+            {
+                constexpr int VEC = S::FC1_VEC, NI = S::NF1 / VEC, NPART = (VEC == 4) ? 2 : 1;
+                constexpr int RP = (S::F1 + NPART - 1) / NPART;
+                if (tid < NI * NPART) {
+                    const int i0 = VEC * (tid % NI), part = tid / NI;
+                    const int r0 = part * RP, r1 = (r0 + RP < S::F1) ? r0 + RP : S::F1;
+                    float acc[VEC];
 #pragma unroll
-                for (int e = 0; e < VEC; ++e) acc[e] = 0.0f;
-                float wa[10][VEC], wb[10][VEC];
-                auto load = [&](float (&w)[10][VEC], int j0) {
+                    for (int e = 0; e < VEC; ++e) acc[e] = 0.0f;
+                    float wa[10][VEC], wb[10][VEC];
+                    auto load = [&](float (&w)[10][VEC], int j0) {
 #pragma unroll
-                    for (int jj = 0; jj < 10; ++jj) {
-                        const int j = j0 + jj;
-                        const float *src = W + S::OF1 + (j < r1 ? j : r0) * S::NF1 + i0;
-                        if (VEC == 4) {
-                            f4 t = *(const f4 *)src;
+                        for (int jj = 0; jj < 10; ++jj) {
+                            const int j = j0 + jj;
+                            const float *src = W + S::OF1 + (j < r1 ? j : r0) * S::NF1 + i0;
+                            if (VEC == 4) {
+                                f4 t = *(const f4 *)src;
 #pragma unroll
-                            for (int e = 0; e < VEC; ++e) w[jj][e] = t[e];
-                        } else {
-                            w[jj][0] = *src;
+                                for (int e = 0; e < VEC; ++e) w[jj][e] = t[e];
+                            } else {
+                                w[jj][0] = *src;
+                            }
+                        }
+                    };
+                    auto comp = [&](const float (&w)[10][VEC], int j0) {
+#pragma unroll
+                        for (int jj = 0; jj < 10; ++jj) {
+                            if (j0 + jj < r1) {
+                                const float d = sm.dh[j0 + jj];
+#pragma unroll
+                                for (int e = 0; e < VEC; ++e) acc[e] = fmaf(w[jj][e], d, acc[e]);
+                            }
+                        }
+                    };
+                    load(wa, r0);
+                    for (int j0 = r0; j0 < r1; j0 += 20) {
+                        if (j0 + 10 < r1) load(wb, j0 + 10);
+                        comp(wa, j0);
+                        if (j0 + 10 < r1) {
+                            if (j0 + 20 < r1) load(wa, j0 + 20);
+                            comp(wb, j0 + 10);
                         }
                     }
-                };
-                auto comp = [&](const float (&w)[10][VEC], int j0) {
+                    float *dst = (part == 0) ? sm.e2 : sm.e2b;
 #pragma unroll
-                    for (int jj = 0; jj < 10; ++jj) {
-                        if (j0 + jj < r1) {
-                            const float d = sm.dh[j0 + jj];
+                    for (int e = 0; e < VEC; ++e) dst[i0 + e] = acc[e];
+                }
+            }
+            __syncthreads();
+            // (wavefront w pushes rows j = w, w + 4, ...; lane l the inputs
+            // l + 64c, so a push instruction covers up to 64 consecutive weights)
+            {
+                constexpr int IC = (S::NF1 + 63) / 64;
+                float xv[IC];
 #pragma unroll
-                            for (int e = 0; e < VEC; ++e) acc[e] = fmaf(w[jj][e], d, acc[e]);
-                        }
-                    }
-                };
-                load(wa, r0);
-                for (int j0 = r0; j0 < r1; j0 += 20) {
-                    if (j0 + 10 < r1) load(wb, j0 + 10);
-                    comp(wa, j0);
-                    if (j0 + 10 < r1) {
-                        if (j0 + 20 < r1) load(wa, j0 + 20);
-                        comp(wb, j0 + 10);
+                for (int c = 0; c < IC; ++c) {
+                    int i = lane + 64 * c;
+                    xv[c] = (i < S::NF1) ? sm.p2[i] : 0.0f;
+                }
+                for (int j = wave; j < S::F1; j += NW) {
+                    const float d = sm.dh[j];
+#pragma unroll
+                    for (int c = 0; c < IC; ++c) {
+                        int i = lane + 64 * c;
+                        if (i < S::NF1) push(S::OF1 + j * S::NF1 + i, d * xv[c]);
                     }
                 }
-                float *dst = (part == 0) ? sm.e2 : sm.e2b;
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) dst[i0 + e] = acc[e];
             }
-        }
-        __syncthreads();
-        // FC1 push; pool2 backward -> dense conv2 deltas; clear e1
-        // (wavefront w pushes rows j = w, w + 4, ...; lane l the inputs
-        // l + 64c, so a push instruction covers up to 64 consecutive weights)
-        {
+            if (tid < S::F1) push(S::OBF1 + tid, sm.dh[tid]);
+        } else {
+            // One pass: each FC1 push returns the weight it updated, this
+            // layer's pre-update weight (Section III-A.2), so the errors
+            // e2[i] = sum_j W[j][i] dh[j] need no separate read of the FC1
+            // weights.  Wavefront w pushes rows j = w, w + 4, ... (lane l the
+            // inputs l + 64c) and keeps a partial sum per input in the free
+            // conv2 output buffer; the pool2 backward below adds the four in
+            // wavefront order.
             constexpr int IC = (S::NF1 + 63) / 64;
-            float xv[IC];
+            float xv[IC], ep[IC];
 #pragma unroll
             for (int c = 0; c < IC; ++c) {
                 int i = lane + 64 * c;
                 xv[c] = (i < S::NF1) ? sm.p2[i] : 0.0f;
+                ep[c] = 0.0f;
             }
-            for (int j = wave; j < S::F1; j += NW) {
-                const float d = sm.dh[j];
+            for (int j = wave; j < S::F1; j += 2 * NW) {
+                const int j2 = j + NW;
+                const float d = sm.dh[j], d2 = (j2 < S::F1) ? sm.dh[j2] : 0.0f;
+                float old[2][IC];
 #pragma unroll
                 for (int c = 0; c < IC; ++c) {
                     int i = lane + 64 * c;
-                    if (i < S::NF1) push(S::OF1 + j * S::NF1 + i, d * xv[c]);
+                    old[0][c] = (i < S::NF1) ? push.with_old(S::OF1 + j * S::NF1 + i, d * xv[c]) : 0.0f;
+                    old[1][c] = (i < S::NF1 && j2 < S::F1)
+                                    ? push.with_old(S::OF1 + j2 * S::NF1 + i, d2 * xv[c]) : 0.0f;
                 }
+#pragma unroll
+                for (int c = 0; c < IC; ++c) ep[c] = fmaf(old[1][c], d2, fmaf(old[0][c], d, ep[c]));
             }
+#pragma unroll
+            for (int c = 0; c < IC; ++c) {
+                int i = lane + 64 * c;
+                if (i < S::NF1) sm.y2[wave * S::NF1 + i] = ep[c];
+            }
+            if (tid < S::F1) push(S::OBF1 + tid, sm.dh[tid]);
         }
-        if (tid < S::F1) push(S::OBF1 + tid, sm.dh[tid]);
+        __syncthreads();
+        // pool2 backward -> dense conv2 deltas; clear e1
         for (int t = tid; t < S::C2P * 96; t += NT) {
             int o = t / 96, p = t - 96 * o;
             float d = 0.0f;
@@ -492,7 +532,11 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 int q = o * S::NP2 + (py / 3) * 3 + px / 3;
                 int w = (py % 3) * 3 + px % 3;
                 if (sm.am2[q] == w) {
-                    const float e = (S::FC1_VEC == 4) ? sm.e2[q] + sm.e2b[q] : sm.e2[q];
+                    float e;
+                    if constexpr (MODE == kForwardBackward)
+                        e = (S::FC1_VEC == 4) ? sm.e2[q] + sm.e2b[q] : sm.e2[q];
+                    else
+                        e = ((sm.y2[q] + sm.y2[S::NF1 + q]) + sm.y2[2 * S::NF1 + q]) + sm.y2[3 * S::NF1 + q];
                     d = e * dact_from_y(sm.p2[q]);
                 }
             }
@@ -528,19 +572,16 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                         const int uv = 4 * (i0 + t) + (lr & 3);
                         wo[t] = (t < nt && uv < 25) ? (c0 + (lr >> 2)) * 25 + uv : -1;
                     }
-                    // every k-step's weights requested at once (one memory
-                    // latency per pass)
-                    float av[S::OKS][TI];
-#pragma unroll
-                    for (int ks = 0; ks < S::OKS; ++ks) {
+                    // the next output maps' weights requested while the
+                    // current ones compute
+                    float aA[TI], aB[TI];
+                    auto load_a = [&](float (&av)[TI], int ks) {
                         const int o = 4 * ks + lg;
                         const float *w2 = W + S::OW2 + (o < S::C2 ? o : 0) * S::KC2;
 #pragma unroll
-                        for (int t = 0; t < TI; ++t)
-                            av[ks][t] = (o < S::C2 && wo[t] >= 0) ? w2[wo[t]] : 0.0f;
-                    }
-#pragma unroll
-                    for (int ks = 0; ks < S::OKS; ++ks) {
+                        for (int t = 0; t < TI; ++t) av[t] = (o < S::C2 && wo[t] >= 0) ? w2[wo[t]] : 0.0f;
+                    };
+                    auto compute = [&](const float (&av)[TI], int ks) {
                         const int o = 4 * ks + lg;
                         float bv[RT2];
 #pragma unroll
@@ -548,7 +589,16 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                         for (int t = 0; t < TI; ++t)
 #pragma unroll
-                            for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[ks][t], bv[j], acc[t][j]);
+                            for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
+                    };
+                    load_a(aA, 0);
+                    for (int ks = 0; ks < S::OKS; ks += 2) {
+                        if (ks + 1 < S::OKS) load_a(aB, ks + 1);
+                        compute(aA, ks);
+                        if (ks + 1 < S::OKS) {
+                            if (ks + 2 < S::OKS) load_a(aA, ks + 2);
+                            compute(aB, ks + 1);
+                        }
                     }
                     float *dp[RT2];
                     bool pvv[RT2];
@@ -751,6 +801,8 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 using Small = Cpcp<5, 10, 50>;
 using Medium = Cpcp<20, 40, 150>;
 static_assert(Small::NPARAM == 6405 && Medium::NPARAM == 76040, "Table I weight counts");
+static_assert(NW * Small::NF1 <= Small::C2 * Small::NY2 && NW * Medium::NF1 <= Medium::C2 * Medium::NY2,
+              "FC1 partial sums fit in the conv2 output buffer");
 static_assert(NW * Small::CT1 * 256 <= Small::C2P * 96 && NW * Medium::CT1 * 256 <= Medium::C2P * 96,
               "conv1 partial tiles fit in the delta buffer");
 
