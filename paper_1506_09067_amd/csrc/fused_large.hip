@@ -47,6 +47,8 @@ constexpr int OF1 = OB3 + C3, OBF1 = OF1 + F1 * NF1;
 constexpr int OF2 = OBF1 + F1, OBF2 = OF2 + F2 * F1;
 constexpr int NPARAM = OBF2 + F2;
 static_assert(NPARAM == 363960, "large net parameter count");
+static_assert(OW2 % 4 == 0 && KC2 % 4 == 0 && OF1 % 4 == 0 && OW3 % 4 == 0 && KC3 % 16 == 0,
+              "16-byte weight loads stay inside one row");
 
 constexpr int NT = 256;   // threads per worker
 constexpr int NW = NT / 64;
@@ -122,10 +124,25 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         }
         const int label = a.labels[idx];
         for (int i = tid; i < NX; i += NT) sm.x[i] = a.x[idx * NX + i];
-        // conv2 weights staged in LDS as [k][o] (o padded to 65 to spread banks)
-        for (int t = tid; t < C2 * KC2; t += NT) {
-            int o = t / KC2, k = t - o * KC2;
-            sm.w2s[k * 65 + o] = W[OW2 + t];
+        // conv2 weights staged in LDS as [k][o] (o padded to 65 to spread
+        // banks): every 16-byte load is issued before the first LDS write
+        {
+            constexpr int N4 = C2 * KC2 / 4, PER = (N4 + NT - 1) / NT;  // 2700 float4
+            f4 wv[PER];
+#pragma unroll
+            for (int q = 0; q < PER; ++q) {
+                const int t4 = tid + NT * q;
+                wv[q] = (t4 < N4) ? *(const f4 *)(W + OW2 + 4 * t4) : f4{0.f, 0.f, 0.f, 0.f};
+            }
+#pragma unroll
+            for (int q = 0; q < PER; ++q) {
+                const int t4 = tid + NT * q;
+                if (t4 < N4) {
+                    const int o = (4 * t4) / KC2, k = 4 * t4 - o * KC2;  // KC2 % 4 == 0: one row
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) sm.w2s[(k + e) * 65 + o] = wv[q][e];
+                }
+            }
         }
         for (int t = tid; t < KC2 * 5; t += NT) {
             int k = t / 5, o = C2 + (t - 5 * k);
@@ -239,7 +256,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         // K = 2160 in 135 super-steps of 16, split 34/34/34/33 over the wavefronts.
         // Within a super-step lane group g holds k = 16S + 4g + s at sub-step s,
         // so each lane reads its four weights of a super-step with one 16-byte
-        // load; the next super-step's weights are loaded while this one computes.
+        // load.
         {
             f4 acc[3][7];
 #pragma unroll
@@ -255,7 +272,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 base[i] = valid[i] ? window_pos(m >> 2, m & 3, 3, H2) : 0;
             }
             const int S0 = wave * 34, S1 = (S0 + 34 < 135) ? S0 + 34 : 135;
-            f4 bA[7], bB[7];
+            f4 bA[7], bB[7], bC[7];
             auto load_b = [&](f4 (&b)[7], int S) {
 #pragma unroll
                 for (int j = 0; j < 7; ++j) {
@@ -278,13 +295,19 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                         for (int j = 0; j < 7; ++j) acc[i][j] = mfma(av[i], b[j][s], acc[i][j]);
                 }
             };
+            // weights two super-steps ahead (a ring of three buffers)
             load_b(bA, S0);
-            for (int S = S0; S < S1; S += 2) {
-                if (S + 1 < S1) load_b(bB, S + 1);
+            if (S0 + 1 < S1) load_b(bB, S0 + 1);
+            for (int S = S0; S < S1; S += 3) {
+                if (S + 2 < S1) load_b(bC, S + 2);
                 compute(bA, S);
                 if (S + 1 < S1) {
-                    if (S + 2 < S1) load_b(bA, S + 2);
+                    if (S + 3 < S1) load_b(bA, S + 3);
                     compute(bB, S + 1);
+                }
+                if (S + 2 < S1) {
+                    if (S + 4 < S1) load_b(bB, S + 4);
+                    compute(bC, S + 2);
                 }
             }
             // fixed-order reduction (w0 + w2) + (w1 + w3) through LDS; the
@@ -587,8 +610,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         // same s2 entries.  Row q of tile i holds input map c0 + q/4 at kernel
         // offset uv = 4i + q%4: in the accumulator the four lane groups then
         // hold four different maps at one (u,v), so no scatter instruction
-        // has two lanes on one address.  The next output maps' weights and
-        // deltas are loaded while the current ones compute.
+        // has two lanes on one address.
         for (int blk = wave; blk < C2 / 4; blk += NW) {
             f4 acc[9][3];
 #pragma unroll
@@ -612,6 +634,8 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                     for (int j = 0; j < 3; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
             };
+            // the next output maps' weights and deltas are loaded while the
+            // current ones compute
             load(aA, bA, 0);
             for (int ks = 0; ks < C3 / 4; ks += 2) {
                 if (ks + 1 < C3 / 4) load(aB, bB, ks + 1);
