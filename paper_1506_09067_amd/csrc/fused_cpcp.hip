@@ -678,13 +678,11 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             for (int i = 0; i < S::CT2; ++i)
 #pragma unroll
                 for (int s = 0; s < 21; ++s) ad[i][s] = sm.d2[(16 * i + lr) * 96 + 4 * s + lg];
-            int pb[21];
-#pragma unroll
-            for (int s = 0; s < 21; ++s) {
-                int p = 4 * s + lg;
-                int py = p / S::H2, px = p - py * S::H2;
-                pb[s] = (p < S::NY2) ? py * S::Q1 + px : -1;
-            }
+            // input offset of output position p = 4s + lg (or -1 past the map)
+            auto pb = [&](int s) {
+                const int p = 4 * s + lg, py = p / S::H2, px = p - py * S::H2;
+                return (p < S::NY2) ? py * S::Q1 + px : -1;
+            };
             // JB column tiles of 16 k per pass, so that JB * CT2 accumulators
             // keep the matrix core busy
             constexpr int NJT = S::KC2P / 16, JB = (NJT / NW >= 4) ? 4 : 2;
@@ -707,7 +705,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 for (int s = 0; s < 21; ++s) {
                     float bv[JB];
 #pragma unroll
-                    for (int b = 0; b < JB; ++b) bv[b] = (kv[b] && pb[s] >= 0) ? pc[b][pb[s]] : 0.0f;
+                    for (int b = 0; b < JB; ++b) {
+                        const int q = pb(s);
+                        bv[b] = (kv[b] && q >= 0) ? pc[b][q] : 0.0f;
+                    }
 #pragma unroll
                     for (int b = 0; b < JB; ++b)
 #pragma unroll
@@ -827,7 +828,7 @@ int cpcp_blocks_per_cu() {
     return nb;
 }
 
-constexpr int kSmallMinBlocks = 2, kMediumMinBlocks = 2;
+constexpr int kSmallMinBlocks = 3, kMediumMinBlocks = 2;
 
 bool matches(const Net &net, int c1, int c2, int f1) {
     const int spec[6][3] = {{kConv, c1, 4}, {kPool, 0, 2}, {kConv, c2, 5},
