@@ -163,6 +163,77 @@ def worker_sweep(chaos, wl, torch):
     return {"sweep": "Hogwild training throughput vs concurrent workers", "nets": out}
 
 
+def model_fit(chaos, wl, torch, name):
+    """Fit the performance model of Section III-C (paper_1506_09067_amd.perfmodel)
+    to this GPU: Training epochs timed at 1, 2, 4, ... workers, the forward
+    rate from the 10,000-sample test set, then MemoryContention(p).  The
+    accuracy alpha is measured two ways: worker counts left out of the fit
+    (every other power of two below the largest), and a whole Training +
+    Validation + Testing session of two epochs at every resident worker.
+    The what-if table is the Table III analog, in seconds, at the resident
+    worker count and at twice that (beyond what the GPU holds)."""
+    from paper_1506_09067_amd import perfmodel as pm
+    layers = wl.NETS[name]
+    p0 = wl.init_params(layers)
+    x, y = wl.train_set(60000)
+    xt, yt = wl.test_set(10000)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    xtd, ytd = torch.from_numpy(xt).cuda(), torch.from_numpy(yt).cuda()
+    flops, fwd = train_flops_per_sample(layers)
+    net = chaos.Net(layers, p0)
+    pmax = net.max_workers
+
+    def timed(fn, reps=1):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / 1e3 / reps
+
+    epochs = {}
+    p = 1
+    while p <= pmax:
+        n = min(60000, max(2000, 500 * p))
+        net.set_params(torch.from_numpy(p0).cuda())
+        secs = timed(lambda: net.train_epoch(xd[:n], yd[:n], 1e-3, workers=p))
+        epochs[p] = (n, secs)
+        p *= 2
+    t_fwd_one = timed(lambda: net.evaluate(xtd, ytd), 3) / 10000 * pmax
+    n1, s1 = epochs[1]
+    ps = sorted(epochs)
+    held = [q for k, q in enumerate(ps) if k % 2 == 1 and q != ps[-1]]  # interior points
+    fit_part = pm.fit(fwd, flops - fwd, s1 / n1, t_fwd_one,
+                      {q: v for q, v in epochs.items() if q not in held})
+    loo = {q: pm.accuracy(epochs[q][1], fit_part.predict_training(epochs[q][0], 1, q))
+           for q in held}
+    model = pm.fit(fwd, flops - fwd, s1 / n1, t_fwd_one, epochs)
+    # a whole session: Training + Validation + Testing, two epochs
+    net.set_params(torch.from_numpy(p0).cuda())
+    sess = timed(lambda: net.train_session(xd, yd, xtd, ytd, 2, 1e-3, 1.0))
+    sess_pred = model.predict(60000, 10000, 2, pmax)
+    table = {}
+    for p in (pmax, 2 * pmax):
+        table[str(p)] = {f"{i // 1000}k/{it // 1000}k": {str(ep): model.predict(i, it, ep, p)
+                                                         for ep in (70, 140, 280, 560)}
+                         for i, it in ((60000, 10000), (120000, 20000), (240000, 40000))}
+    return {
+        "model": "Section III-C, refitted on MI355X", "net": name, "resident_workers": pmax,
+        "FProp": fwd, "BProp": flops - fwd, "s_flop_per_s": pm.PEAK_FP32_PER_CU,
+        "penalty_train": model.penalty_train, "penalty_fwd": model.penalty_fwd,
+        "t_train_one_worker_s": model.t_train(), "t_fwd_one_worker_s": model.t_fwd(),
+        "memory_contention_s": {str(q): v for q, v in model.contention.items()},
+        "measured_training_epochs": {str(q): {"samples": n, "seconds": t} for q, (n, t) in epochs.items()},
+        "alpha_left_out_pct": {str(q): v for q, v in loo.items()},
+        "session_2_epochs": {"measured_s": sess, "predicted_s": sess_pred,
+                             "alpha_pct": pm.accuracy(sess, sess_pred)},
+        "what_if_seconds": table,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -178,6 +249,10 @@ def main():
                     help="instead of the benchmark line, print one JSON line with training "
                          "throughput against the number of Hogwild workers for the small, "
                          "medium and large nets")
+    ap.add_argument("--model", action="store_true",
+                    help="instead of the benchmark line, fit the Section III-C performance "
+                         "model to measurements of --net and print its parameters, its "
+                         "prediction accuracy and a what-if table as one JSON line")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (calibrates "
                          "the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -203,6 +278,9 @@ def main():
     torch.cuda.set_device(0)
     if args.sweep:
         print(json.dumps(worker_sweep(chaos, wl, torch)), flush=True)
+        return
+    if args.model:
+        print(json.dumps(model_fit(chaos, wl, torch, args.net)), flush=True)
         return
     layers = wl.NETS[args.net]
     p0 = wl.init_params(layers)
