@@ -32,8 +32,10 @@ On the GPU a processing unit is one Hogwild worker.  The refit takes
   * MemoryContention(p): from the measured Training epoch time at p workers,
     the excess over T_comp per round of p images.
 Prediction at a worker count that was not measured interpolates
-MemoryContention linearly in log p (and holds the last measured value
-beyond the largest p).  The prediction accuracy is the paper's
+MemoryContention linearly in log p; beyond the largest measured p it
+continues the power law of the last measured interval (contention grows
+steeply once the update stream saturates), below the smallest it holds the
+first value.  The prediction accuracy is the paper's
 alpha = |measured - predicted| / predicted * 100 %.
 
 Pure Python: no GPU code; bench.py --model supplies the measurements.
@@ -86,7 +88,11 @@ class Model:
         if p <= ps[0]:
             return self.contention[ps[0]]
         if p >= ps[-1]:
-            return self.contention[ps[-1]]
+            last = self.contention[ps[-1]]
+            if len(ps) > 1 and last > 0 and self.contention[ps[-2]] > 0 and p > ps[-1]:
+                k = math.log(last / self.contention[ps[-2]]) / math.log(ps[-1] / ps[-2])
+                return last * (p / ps[-1]) ** max(k, 0.0)
+            return last
         for lo, hi in zip(ps, ps[1:]):
             if lo <= p <= hi:
                 w = (math.log(p) - math.log(lo)) / (math.log(hi) - math.log(lo))

@@ -53,12 +53,18 @@ def test_memory_term_follows_the_formula():
     assert m.t_mem(60000, 15, 4) == pytest.approx(2e-3 * 60000 * 15 / 4)
 
 
-def test_contention_interpolates_in_log_p_and_holds_outside():
+def test_contention_interpolates_in_log_p_and_extrapolates_the_last_power_law():
     m = pm.Model(fprop=1.0, bprop=1.0, contention={4: 1.0, 64: 3.0})
-    assert m.memory_contention(2) == 1.0
-    assert m.memory_contention(512) == 3.0
+    assert m.memory_contention(2) == 1.0                  # held below the first point
     assert m.memory_contention(16) == pytest.approx(2.0)  # halfway in log p
     assert m.memory_contention(8) == pytest.approx(1.5)
+    # beyond the last point: MC grows as p^k with k from the last interval
+    k = math.log(3.0) / math.log(16.0)
+    assert m.memory_contention(128) == pytest.approx(3.0 * 2 ** k)
+    assert m.memory_contention(1024) == pytest.approx(3.0 * 16 ** k)
+    # a vanishing first value cannot define a power law: hold
+    flat = pm.Model(fprop=1.0, bprop=1.0, contention={4: 0.0, 64: 3.0})
+    assert flat.memory_contention(256) == 3.0
 
 
 def test_fit_recovers_planted_parameters():
