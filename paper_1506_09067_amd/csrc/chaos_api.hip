@@ -21,6 +21,7 @@ struct chaos_net {
     float *params = nullptr;      // shared weights, canonical layout
     int block = 256;              // threads per worker
     bool fused = false;           // the fused large-net kernel serves this net
+    bool t1 = false;              // the fused kernel of Table I's large net serves this net
     int cpcp = 0;                 // fused small (1) / medium (2) kernel serves this net
     int max_workers = 0;          // resident workers of the training kernel
     float *scratch = nullptr;     // [max_workers][scratch_floats]
@@ -180,6 +181,7 @@ chaos::WorkArgs base_args(chaos_net *net, const float *x, const int32_t *labels,
 
 hipError_t launch(chaos_net *net, int mode, const chaos::WorkArgs &a, int grid, hipStream_t s) {
     if (net->fused) return chaos::launch_fused_large(mode, a, grid, s);
+    if (net->t1) return chaos::launch_fused_t1(mode, a, grid, s);
     if (net->cpcp) return chaos::launch_fused_cpcp(net->cpcp, mode, a, grid, s);
     return chaos::launch_worker(mode, net->desc, a, grid, net->block, s);
 }
@@ -212,15 +214,17 @@ int chaos_create_net(int32_t in_h, int32_t in_w, const chaos_layer *layers, int3
     if (e != hipSuccess) { delete net; return hip_fail(e, "device query"); }
     net->block = 256;
     net->fused = chaos::fused_large_matches(desc);
-    net->cpcp = net->fused ? 0 : chaos::fused_cpcp_variant(desc);
+    net->t1 = !net->fused && chaos::fused_t1_matches(desc);
+    net->cpcp = (net->fused || net->t1) ? 0 : chaos::fused_cpcp_variant(desc);
     int per_cu = net->fused ? chaos::fused_large_blocks_per_cu()
+               : net->t1    ? chaos::fused_t1_blocks_per_cu()
                : net->cpcp  ? chaos::fused_cpcp_blocks_per_cu(net->cpcp)
                             : chaos::worker_blocks_per_cu(net->block);
     if (per_cu < 1) { delete net; return fail(CHAOS_EDEVICE, "occupancy query failed"); }
     net->max_workers = per_cu * cus;
     net->worker_limit = std::max(net->max_workers, chaos::worker_blocks_per_cu(64) * cus);
     // the fused kernels keep every per-sample value in LDS: no scratch
-    size_t scratch_bytes = (net->fused || net->cpcp)
+    size_t scratch_bytes = (net->fused || net->t1 || net->cpcp)
                                ? 0
                                : (size_t)net->max_workers * desc.scratch_floats * sizeof(float);
     e = hipMalloc(&net->params, (size_t)n_params * sizeof(float));

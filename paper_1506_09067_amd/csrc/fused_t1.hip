@@ -1,0 +1,966 @@
+// Fused per-sample CHAOS worker for the large net of Table I:
+//   1x29x29 -> conv 20@4x4 -> (max 1x1: the identity) -> conv 60@5x5
+//           -> max 2 -> conv 100@6x6 -> max 2 -> FC 150 -> FC 10,
+// activation 1.7159 tanh(2z/3) on every conv/FC.
+//
+// Organised like the kernel of the smaller large net (fused_large.hip): one
+// workgroup of 4 wavefronts per worker, persistent, every per-sample value in
+// LDS, the convolutions as implicit GEMMs on the fp32 matrix cores.  From
+// conv3 on the two nets are the same, and so is that part of this kernel.
+// What differs is the front: conv1 is not pooled (26x26 maps), conv2 works on
+// them with 5x5 kernels (22x22 outputs, 64 % of the MACs) and is pooled 2x2
+// in its epilogue.  LDS is reused across phases: region A holds the conv1
+// output in the forward pass, then the conv3 split-K partials, the conv3
+// backward buffers, the conv1 output again (recomputed for the conv2 weight
+// gradient, then turned into f'), and last the conv1 partial gradient tiles;
+// region B holds the pool2/FC1 values, then the conv1 output errors.
+#include <type_traits>
+
+#include "chaos_internal.h"
+#include "device_common.h"
+
+namespace chaos {
+namespace {
+
+// ---- shapes of the Table I large net ----------------------------------------
+constexpr int IN = 29, NX = IN * IN;            // input 1x29x29
+constexpr int C1 = 20, H1 = 26, NA1 = H1 * H1;  // conv1 20@26x26 (K = 16)
+constexpr int C2 = 60, K2 = 5, H2F = 22;        // conv2 60@22x22 on 20@26x26
+constexpr int KC2 = C1 * K2 * K2;               // 500
+constexpr int KC2P = 512;                       // K padded to whole 16-k super-steps
+constexpr int Q2 = 11, NY2 = Q2 * Q2;           // pool 2 -> 60@11x11 (conv3 input)
+constexpr int M2 = 4 * NY2, M2T = 31;           // conv2 outputs in (pooled position, window
+                                                // element) order: 484 rows, 31 tiles
+constexpr int H2 = Q2;                          // width of the conv3 input maps
+constexpr int C3 = 100, K3 = 6;                 // conv3 100@6x6 on 60@11x11
+constexpr int KC3 = C2 * K3 * K3;               // 2160
+constexpr int NP3 = 9;                          // pool 2 -> 3x3
+constexpr int NF1 = C3 * NP3;                   // 900 inputs of FC1
+constexpr int F1 = 150, F2 = 10;
+
+// canonical parameter offsets
+constexpr int OW1 = 0, OB1 = OW1 + C1 * 16;
+constexpr int OW2 = OB1 + C1, OB2 = OW2 + C2 * KC2;
+constexpr int OW3 = OB2 + C2, OB3 = OW3 + C3 * KC3;
+constexpr int OF1 = OB3 + C3, OBF1 = OF1 + F1 * NF1;
+constexpr int OF2 = OBF1 + F1, OBF2 = OF2 + F2 * F1;
+constexpr int NPARAM = OBF2 + F2;
+static_assert(NPARAM == 383160, "Table I large net weight count");
+static_assert(OW2 % 4 == 0 && KC2 % 4 == 0 && OF1 % 4 == 0 && OW3 % 4 == 0 && KC3 % 16 == 0,
+              "16-byte weight loads stay inside one row");
+
+constexpr int NT = 256;   // threads per worker
+constexpr int NW = NT / 64;
+
+// conv3 output rows m = 4 * P + w (P pooled 3x3 position, w window element)
+constexpr int M3 = 36, M3P = 48;                // padded to 3 tiles of 16
+
+struct alignas(16) Smem {
+    float x[NX + 3];
+    union {                              // region A
+        float a1[C1 * NA1];              // conv1 output; later f'(conv1 output)
+        float red3[2 * 21 * 256];        // conv3 split-K partial sums (forward)
+        struct {
+            float s2[C2 * NY2];          // conv3 backward-data sums
+            float d3[C3 * M3P];          // conv3 output deltas, rows (P, w)
+        };
+        float red1[NW * 2 * 256];        // conv1 partial gradient tiles
+    };
+    union {                              // region B
+        struct {
+            alignas(16) float p3[NF1];   // pool2 output (FC1 input)
+            alignas(16) float e3[NF1];   // dE/d(pool2 output)
+            float fcpart[NW * NF1];      // FC1 backward partial sums per wavefront
+        };
+        float e1[C1 * NA1];              // dE/d(conv1 output), then conv1 deltas
+    };
+    float y2[C2 * NY2];                  // pooled conv2 output (conv3 input), then its deltas
+    unsigned char am2[C2 * NY2 + 4];     // pool after conv2: argmax (window element 0..3)
+    float h[F1 + 10], dh[F1 + 10];
+    float o[16], dout[16];
+    alignas(16) int koff3[KC3];          // im2col offset into y2 of k = (c,u,v), conv3
+    alignas(16) int koff2[KC2P];         // im2col offset into a1 of k = (c,u,v), conv2 (0 past KC2)
+    unsigned char am3[NF1 + 4];          // pool2 argmax
+    int64_t idx;
+};
+static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
+
+template <int MODE>
+__global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
+    __shared__ Smem sm;
+    const float *W = a.params;
+    constexpr bool kTrain = (MODE == kTrainAtomic || MODE == kTrainRacy);
+
+    // sample-invariant im2col offset tables
+    for (int k = threadIdx.x; k < KC3; k += NT) {
+        int c = k / 36, uv = k - 36 * c, u = uv / 6, v = uv - 6 * u;
+        sm.koff3[k] = c * NY2 + u * H2 + v;
+    }
+    for (int k = threadIdx.x; k < KC2P; k += NT) {
+        int c = k / 25, uv = k - 25 * c, u = uv / 5, v = uv - 5 * u;
+        sm.koff2[k] = (k < KC2) ? c * NA1 + u * H1 + v : 0;
+    }
+
+    for (int64_t step = 0;; ++step) {
+        // opaque thread index: keeps per-phase index arithmetic inside its phase
+        int tid_l = threadIdx.x;
+        asm volatile("" : "+v"(tid_l));
+        const int tid = tid_l, lane = tid_l & 63, lr = lane & 15, lg = lane >> 4;
+        const int wave = __builtin_amdgcn_readfirstlane(tid_l >> 6);
+        // ---- claim a sample (Section III-A.1) ----
+        if (tid == 0) sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1)
+                                      : (int64_t)blockIdx.x + step * gridDim.x;
+        // Reads are on demand: one wavefront drops the weights this CU and its
+        // L2 hold from earlier samples before any weight of this sample is read
+        // (the barrier orders every wavefront's reads after it); the previous
+        // sample's last barrier waited for all of this worker's pushes.
+        if (kTrain && wave == 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        __syncthreads();
+        const int64_t idx = sm.idx;
+        if (idx >= a.n) break;
+        if (kTrain) {
+            if (a.claims && tid == 0) atomicAdd(a.claims + idx, 1);
+        }
+        const int label = a.labels[idx];
+        for (int i = tid; i < NX; i += NT) sm.x[i] = a.x[idx * NX + i];
+        __syncthreads();
+
+        // conv1 (no pooling): rows = the 676 output positions (43 tiles), cols
+        // o < 20, K = 16; a wavefront's tiles i = wave + 4q, six at a time.
+        // Also used to recompute the output for the conv2 weight gradient.
+        auto conv1_forward = [&]() {
+            float bw[4][2], b1[2];
+#pragma unroll
+            for (int s = 0; s < 4; ++s)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) {
+                    int o = 16 * j + lr;
+                    bw[s][j] = (o < C1) ? W[OW1 + o * 16 + 4 * s + lg] : 0.0f;
+                }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) b1[j] = (16 * j + lr < C1) ? W[OB1 + 16 * j + lr] : 0.0f;
+            for (int i0 = wave; i0 < 43; i0 += 6 * NW) {
+                f4 acc[6][2];
+                int base[6];
+#pragma unroll
+                for (int q = 0; q < 6; ++q) {
+                    int m = 16 * (i0 + 4 * q) + lr;
+                    int my = m / H1, mx = m - my * H1;
+                    base[q] = (m < NA1) ? my * IN + mx : 0;
+                    acc[q][0] = f4{0.f, 0.f, 0.f, 0.f};
+                    acc[q][1] = acc[q][0];
+                }
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+#pragma unroll
+                    for (int q = 0; q < 6; ++q) {
+                        float av = sm.x[base[q] + s * IN + lg];
+                        acc[q][0] = mfma(av, bw[s][0], acc[q][0]);
+                        acc[q][1] = mfma(av, bw[s][1], acc[q][1]);
+                    }
+#pragma unroll
+                for (int q = 0; q < 6; ++q)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        int m = 16 * (i0 + 4 * q) + 4 * lg + r;
+                        if (m >= NA1) continue;
+#pragma unroll
+                        for (int j = 0; j < 2; ++j) {
+                            int o = 16 * j + lr;
+                            if (o < C1) sm.a1[o * NA1 + m] = act_y(acc[q][j][r] + b1[j]);
+                        }
+                    }
+            }
+        };
+
+        // ================= forward propagation =================
+        conv1_forward();
+        __syncthreads();
+
+        // conv2 + pool: rows m = 4P + w (P < 121 pooled positions, w window
+        // element: one lane's four accumulators are one 2x2 window), 31 tiles;
+        // wavefront w takes output maps 16w..16w+15 (one column tile) for all
+        // rows; K = 500 (padded to 512) in super-steps of 16, lane group g
+        // holding k = 16S + 4g + e at sub-step e, so its four weights of a
+        // super-step are one 16-byte load, requested two super-steps ahead.
+        {
+            const int o = 16 * wave + lr;
+            const bool ov = o < C2;
+            const float *wrow = W + OW2 + (ov ? o : 0) * KC2 + 4 * lg;
+            int base[M2T];
+#pragma unroll
+            for (int i = 0; i < M2T; ++i) {
+                const int m = 16 * i + lr, P = m >> 2, w = m & 3;
+                const int py = P / Q2, px = P - py * Q2;
+                base[i] = (m < M2) ? (2 * py + (w >> 1)) * H1 + 2 * px + (w & 1) : 0;
+            }
+            f4 acc[M2T];
+#pragma unroll
+            for (int i = 0; i < M2T; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+            auto load = [&](int S) {
+                return (ov && 16 * S + 4 * lg < KC2) ? *(const f4 *)(wrow + 16 * S)
+                                                     : f4{0.f, 0.f, 0.f, 0.f};
+            };
+            auto compute = [&](f4 b, int S) {
+                const int4 ko = *(const int4 *)(sm.koff2 + 16 * S + 4 * lg);
+                const int offs[4] = {ko.x, ko.y, ko.z, ko.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int i = 0; i < M2T; ++i) acc[i] = mfma(sm.a1[base[i] + offs[e]], b[e], acc[i]);
+            };
+            constexpr int NS = KC2P / 16;  // 32
+            f4 bA = load(0), bB = load(1), bC;
+            for (int S = 0; S < NS; S += 3) {
+                if (S + 2 < NS) bC = load(S + 2);
+                compute(bA, S);
+                if (S + 1 < NS) {
+                    if (S + 3 < NS) bA = load(S + 3);
+                    compute(bB, S + 1);
+                }
+                if (S + 2 < NS) {
+                    if (S + 4 < NS) bB = load(S + 4);
+                    compute(bC, S + 2);
+                }
+            }
+            if (ov) {
+                const float bias = W[OB2 + o];
+#pragma unroll
+                for (int i = 0; i < M2T; ++i) {
+                    const int P = 4 * i + lg;
+                    if (P < NY2) {
+                        float ym;
+                        int ag;
+                        pool4(acc[i], bias, ym, ag);
+                        sm.y2[o * NY2 + P] = ym;
+                        sm.am2[o * NY2 + P] = (unsigned char)ag;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+
+        // conv3 + pool2: rows m = 4P + w (36 -> 3 tiles), cols o < 100 (7 tiles),
+        // K = 2160 in 135 super-steps of 16, split 34/34/34/33 over the wavefronts.
+        // Within a super-step lane group g holds k = 16S + 4g + s at sub-step s,
+        // so each lane reads its four weights of a super-step with one 16-byte
+        // load.
+        {
+            f4 acc[3][7];
+#pragma unroll
+            for (int i = 0; i < 3; ++i)
+#pragma unroll
+                for (int j = 0; j < 7; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+            int base[3];
+            bool valid[3];
+#pragma unroll
+            for (int i = 0; i < 3; ++i) {
+                int m = 16 * i + lr;
+                valid[i] = m < M3;
+                base[i] = valid[i] ? window_pos(m >> 2, m & 3, 3, H2) : 0;
+            }
+            const int S0 = wave * 34, S1 = (S0 + 34 < 135) ? S0 + 34 : 135;
+            f4 bA[7], bB[7], bC[7];
+            auto load_b = [&](f4 (&b)[7], int S) {
+#pragma unroll
+                for (int j = 0; j < 7; ++j) {
+                    int o = 16 * j + lr;
+                    b[j] = (o < C3) ? *(const f4 *)(W + OW3 + o * KC3 + 16 * S + 4 * lg)
+                                    : f4{0.f, 0.f, 0.f, 0.f};
+                }
+            };
+            auto compute = [&](const f4 (&b)[7], int S) {
+                const int4 ko = *(const int4 *)(sm.koff3 + 16 * S + 4 * lg);
+                const int offs[4] = {ko.x, ko.y, ko.z, ko.w};
+#pragma unroll
+                for (int s = 0; s < 4; ++s) {
+                    float av[3];
+#pragma unroll
+                    for (int i = 0; i < 3; ++i) av[i] = valid[i] ? sm.y2[base[i] + offs[s]] : 0.0f;
+#pragma unroll
+                    for (int i = 0; i < 3; ++i)
+#pragma unroll
+                        for (int j = 0; j < 7; ++j) acc[i][j] = mfma(av[i], b[j][s], acc[i][j]);
+                }
+            };
+            // weights two super-steps ahead (a ring of three buffers)
+            load_b(bA, S0);
+            if (S0 + 1 < S1) load_b(bB, S0 + 1);
+            for (int S = S0; S < S1; S += 3) {
+                if (S + 2 < S1) load_b(bC, S + 2);
+                compute(bA, S);
+                if (S + 1 < S1) {
+                    if (S + 3 < S1) load_b(bA, S + 3);
+                    compute(bB, S + 1);
+                }
+                if (S + 2 < S1) {
+                    if (S + 4 < S1) load_b(bB, S + 4);
+                    compute(bC, S + 2);
+                }
+            }
+            // fixed-order reduction (w0 + w2) + (w1 + w3) through LDS; the
+            // epilogue of col tiles 0..3 runs on wavefront 0, of 4..6 on 1
+            float *buf = sm.red3;  // 2 x 21 tiles x 64 lanes x 4 floats
+            if (wave >= 2) {
+                float *dst = buf + (wave - 2) * (21 * 256);
+#pragma unroll
+                for (int i = 0; i < 3; ++i)
+#pragma unroll
+                    for (int j = 0; j < 7; ++j)
+                        *(f4 *)(dst + ((i * 7 + j) * 64 + lane) * 4) = acc[i][j];
+            }
+            __syncthreads();
+            if (wave < 2) {
+                const float *src = buf + wave * (21 * 256);
+#pragma unroll
+                for (int i = 0; i < 3; ++i)
+#pragma unroll
+                    for (int j = 0; j < 7; ++j)
+                        acc[i][j] += *(const f4 *)(src + ((i * 7 + j) * 64 + lane) * 4);
+            }
+            __syncthreads();
+            if (wave < 2) {
+                // wavefront 0 hands over tiles 4..6, wavefront 1 tiles 0..3
+#pragma unroll
+                for (int i = 0; i < 3; ++i)
+#pragma unroll
+                    for (int j = 0; j < 7; ++j)
+                        if ((j >= 4) == (wave == 0))
+                            *(f4 *)(buf + ((i * 7 + j) * 64 + lane) * 4) = acc[i][j];
+            }
+            __syncthreads();
+            if (wave < 2) {
+#pragma unroll
+                for (int j = 0; j < 7; ++j) {
+                    if ((j >= 4) != (wave == 1)) continue;
+                    int o = 16 * j + lr;
+                    if (o >= C3) continue;
+                    float bias = W[OB3 + o];
+#pragma unroll
+                    for (int i = 0; i < 3; ++i) {
+                        f4 t = acc[i][j] + *(const f4 *)(buf + ((i * 7 + j) * 64 + lane) * 4);
+                        int P = 4 * i + lg;
+                        if (P < NP3) {
+                            float ym;
+                            int ag;
+                            pool4(t, bias, ym, ag);
+                            sm.p3[o * NP3 + P] = ym;
+                            sm.am3[o * NP3 + P] = (unsigned char)ag;
+                        }
+                    }
+                }
+            }
+        }
+        __syncthreads();
+
+        // FC1: wavefront w computes neurons [38w, 38w + 38), eight at a time.
+        // Lane l holds inputs 4l + 256c (c < 4) and reads four consecutive
+        // weights of a row with one 16-byte load; the next eight rows are
+        // requested before the current ones are reduced.  The eight partial
+        // sums of a lane are reduced by halving: after exchanges with lanes
+        // l^32, l^16 and l^8 each lane keeps one neuron, and l^4, l^2, l^1
+        // complete its sum.
+        {
+            f4 xin[4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                int i = 4 * lane + 256 * c;
+                xin[c] = (i < NF1) ? *(const f4 *)(sm.p3 + i) : f4{0.f, 0.f, 0.f, 0.f};
+            }
+            const int jb = 38 * wave, je = (jb + 38 < F1) ? jb + 38 : F1;
+            f4 wv[8][4];
+            auto load_rows = [&](int j0) {
+#pragma unroll
+                for (int q = 0; q < 8; ++q)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        int j = j0 + q, i = 4 * lane + 256 * c;
+                        wv[q][c] = (j < je && i < NF1) ? *(const f4 *)(W + OF1 + j * NF1 + i)
+                                                       : f4{0.f, 0.f, 0.f, 0.f};
+                    }
+            };
+            const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+            load_rows(jb);
+            for (int j0 = jb; j0 < je; j0 += 8) {
+                float sq[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    float t = 0.0f;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        t = fmaf(wv[q][c].x, xin[c].x, t);
+                        t = fmaf(wv[q][c].y, xin[c].y, t);
+                        t = fmaf(wv[q][c].z, xin[c].z, t);
+                        t = fmaf(wv[q][c].w, xin[c].w, t);
+                    }
+                    sq[q] = t;
+                }
+                if (j0 + 8 < je) load_rows(j0 + 8);
+                float t4[4], t2[2];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    t4[q] = (b5 ? sq[q + 4] : sq[q]) + __shfl_xor(b5 ? sq[q] : sq[q + 4], 32, 64);
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+                    t2[q] = (b4 ? t4[q + 2] : t4[q]) + __shfl_xor(b4 ? t4[q] : t4[q + 2], 16, 64);
+                float t1 = (b3 ? t2[1] : t2[0]) + __shfl_xor(b3 ? t2[0] : t2[1], 8, 64);
+                t1 += __shfl_xor(t1, 4, 64);
+                t1 += __shfl_xor(t1, 2, 64);
+                t1 += __shfl_xor(t1, 1, 64);
+                const int j = j0 + ((lane >> 3) & 7);
+                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[OBF1 + j]);
+            }
+        }
+        __syncthreads();
+        // FC2 (output layer)
+        for (int j = wave; j < F2; j += NW) {
+            const float *wj = W + OF2 + j * F1;
+            float s = 0.0f;
+#pragma unroll
+            for (int it = 0; it < 3; ++it) {
+                int i = lane + 64 * it;
+                if (i < F1) s = fmaf(wj[i], sm.h[i], s);
+            }
+            s = wave_sum(s);
+            if (lane == 0) sm.o[j] = act_y(s + W[OBF2 + j]);
+        }
+        __syncthreads();
+        if (a.out && tid < F2) a.out[idx * F2 + tid] = sm.o[tid];
+
+        if (MODE == kEvaluate) {
+            if (tid == 0) {
+                int best = 0;
+                for (int k = 1; k < F2; ++k)
+                    if (sm.o[k] > sm.o[best]) best = k;
+                if (best != label) atomicAdd(a.n_wrong, 1);
+            }
+            __syncthreads();
+            continue;
+        }
+
+        // ================= back-propagation =================
+        Push push;
+        push.mode = MODE;
+        push.params = a.params;
+        push.neg_lr = -a.lr;
+        push.each = a.grad_each ? a.grad_each + idx * (int64_t)NPARAM : nullptr;
+        push.part = a.grad_part ? a.grad_part + (int64_t)blockIdx.x * NPARAM : nullptr;
+
+        // output layer: E = 1/2 sum (y - t)^2, delta = (y - t) f'(z)
+        if (tid < 64) {
+            float e = 0.0f;
+            if (tid < F2) {
+                float y = sm.o[tid];
+                float d = y - (tid == label ? 1.0f : 0.0f);
+                e = d * d;
+                sm.dout[tid] = d * dact_from_y(y);
+            }
+            e = wave_sum(e);
+            if (tid == 0 && a.loss) a.loss[idx] = 0.5f * e;
+        }
+        __syncthreads();
+        // FC2 backward data (pre-update weights)
+        if (tid < F1) {
+            float wv[F2];
+#pragma unroll
+            for (int j = 0; j < F2; ++j) wv[j] = W[OF2 + j * F1 + tid];
+            float s = 0.0f;
+#pragma unroll
+            for (int j = 0; j < F2; ++j) s = fmaf(wv[j], sm.dout[j], s);
+            sm.dh[tid] = s * dact_from_y(sm.h[tid]);
+        }
+        __syncthreads();
+        // FC2 push.  FC1 push and FC1 backward data in one pass: each push
+        // returns the weight it updated, which is this layer's pre-update
+        // weight (Section III-A.2), so e3[i] = sum_j W[j][i] dh[j] needs no
+        // separate read of the 540 KB of FC1 weights.  Wavefront w pushes
+        // rows j = w, w + 4, ... (lane l the inputs l + 64c, a push
+        // instruction covers 64 consecutive weights) and keeps a partial sum
+        // per input; the four partial sums are added in wavefront order.
+        for (int t = tid; t < F2 * F1; t += NT) {
+            int j = t / F1, i = t - j * F1;
+            push(OF2 + t, sm.dout[j] * sm.h[i]);
+        }
+        if (tid < F2) push(OBF2 + tid, sm.dout[tid]);
+        if (tid < F1) push(OBF1 + tid, sm.dh[tid]);
+        if constexpr (MODE == kForwardBackward) {
+            // frozen weights: read them (16-byte loads, ten rows per batch,
+            // the next batch requested while this one is summed), then push
+            if (tid < NF1 / 4) {
+                f4 acc = {0.f, 0.f, 0.f, 0.f};
+                f4 wa[10], wb[10];
+                auto load = [&](f4 (&w)[10], int j0) {
+#pragma unroll
+                    for (int jj = 0; jj < 10; ++jj)
+                        w[jj] = *(const f4 *)(W + OF1 + (j0 + jj) * NF1 + 4 * tid);
+                };
+                auto comp = [&](const f4 (&w)[10], int j0) {
+#pragma unroll
+                    for (int jj = 0; jj < 10; ++jj) {
+                        float d = sm.dh[j0 + jj];
+                        acc.x = fmaf(w[jj].x, d, acc.x);
+                        acc.y = fmaf(w[jj].y, d, acc.y);
+                        acc.z = fmaf(w[jj].z, d, acc.z);
+                        acc.w = fmaf(w[jj].w, d, acc.w);
+                    }
+                };
+                load(wa, 0);
+                for (int j0 = 0; j0 < F1; j0 += 20) {
+                    if (j0 + 10 < F1) load(wb, j0 + 10);
+                    comp(wa, j0);
+                    if (j0 + 10 < F1) {
+                        if (j0 + 20 < F1) load(wa, j0 + 20);
+                        comp(wb, j0 + 10);
+                    }
+                }
+                *(f4 *)(sm.e3 + 4 * tid) = acc;
+            }
+            {
+                float xv[15];
+#pragma unroll
+                for (int c = 0; c < 15; ++c) {
+                    int i = lane + 64 * c;
+                    xv[c] = (i < NF1) ? sm.p3[i] : 0.0f;
+                }
+                for (int j = wave; j < F1; j += NW) {
+                    const float d = sm.dh[j];
+#pragma unroll
+                    for (int c = 0; c < 15; ++c) {
+                        int i = lane + 64 * c;
+                        if (i < NF1) push(OF1 + j * NF1 + i, d * xv[c]);
+                    }
+                }
+            }
+        } else {
+            {
+                float xv[15], ep[15];
+#pragma unroll
+                for (int c = 0; c < 15; ++c) {
+                    int i = lane + 64 * c;
+                    xv[c] = (i < NF1) ? sm.p3[i] : 0.0f;
+                    ep[c] = 0.0f;
+                }
+                // two rows per step: 30 pushes in flight before their returns are used
+                for (int j = wave; j < F1; j += 2 * NW) {
+                    const int j2 = j + NW;
+                    const float d = sm.dh[j], d2 = (j2 < F1) ? sm.dh[j2] : 0.0f;
+                    float old[2][15];
+#pragma unroll
+                    for (int c = 0; c < 15; ++c) {
+                        int i = lane + 64 * c;
+                        old[0][c] = (i < NF1) ? push.with_old(OF1 + j * NF1 + i, d * xv[c]) : 0.0f;
+                    }
+                    if (j2 < F1) {
+#pragma unroll
+                        for (int c = 0; c < 15; ++c) {
+                            int i = lane + 64 * c;
+                            old[1][c] = (i < NF1) ? push.with_old(OF1 + j2 * NF1 + i, d2 * xv[c]) : 0.0f;
+                        }
+                    } else {
+#pragma unroll
+                        for (int c = 0; c < 15; ++c) old[1][c] = 0.0f;
+                    }
+#pragma unroll
+                    for (int c = 0; c < 15; ++c) ep[c] = fmaf(old[1][c], d2, fmaf(old[0][c], d, ep[c]));
+                }
+                float *part = sm.fcpart;  // [wavefront][input]
+#pragma unroll
+                for (int c = 0; c < 15; ++c) {
+                    int i = lane + 64 * c;
+                    if (i < NF1) part[wave * NF1 + i] = ep[c];
+                }
+            }
+        }
+        __syncthreads();
+        // e3 = the partial sums in wavefront order (training); pool2
+        // backward -> conv3 output deltas d3[o][4P + w]; clear s2
+        if constexpr (MODE != kForwardBackward) {
+            const float *part = sm.fcpart;
+            for (int q = tid; q < NF1; q += NT)
+                sm.e3[q] = ((part[q] + part[NF1 + q]) + part[2 * NF1 + q]) + part[3 * NF1 + q];
+            __syncthreads();
+        }
+        for (int t = tid; t < C3 * M3P; t += NT) {
+            int o = t / M3P, m = t - o * M3P;
+            float d = 0.0f;
+            if (m < M3) {
+                int P = m >> 2, w = m & 3, q = o * NP3 + P;
+                if (sm.am3[q] == w) d = sm.e3[q] * dact_from_y(sm.p3[q]);
+            }
+            sm.d3[t] = d;
+        }
+        for (int t = tid; t < C2 * NY2; t += NT) sm.s2[t] = 0.0f;
+        __syncthreads();
+
+        // conv3 backward data: C[k][m] = sum_o W3[o][k] d3[o][m], k = (c,u,v);
+        // col2im into s2[c][pos(m) + (u,v)].  Wavefront w owns input maps in
+        // blocks of 4 (144 rows = 9 tiles), so no two wavefronts touch the
+        // same s2 entries.  Row q of tile i holds input map c0 + q/4 at kernel
+        // offset uv = 4i + q%4: in the accumulator the four lane groups then
+        // hold four different maps at one (u,v), so no scatter instruction
+        // has two lanes on one address.
+        for (int blk = wave; blk < C2 / 4; blk += NW) {
+            f4 acc[9][3];
+#pragma unroll
+            for (int i = 0; i < 9; ++i)
+#pragma unroll
+                for (int j = 0; j < 3; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+            const int k0 = blk * 144;
+            const int arow = k0 + (lr >> 2) * 36 + (lr & 3);
+            float aA[9], aB[9], bA[3], bB[3];
+            auto load = [&](float (&av)[9], float (&bv)[3], int ks) {
+                const float *w3 = W + OW3 + (4 * ks + lg) * KC3 + arow;
+#pragma unroll
+                for (int i = 0; i < 9; ++i) av[i] = w3[4 * i];
+                const float *dd = sm.d3 + (4 * ks + lg) * M3P + lr;
+#pragma unroll
+                for (int j = 0; j < 3; ++j) bv[j] = dd[16 * j];
+            };
+            auto compute = [&](const float (&av)[9], const float (&bv)[3]) {
+#pragma unroll
+                for (int i = 0; i < 9; ++i)
+#pragma unroll
+                    for (int j = 0; j < 3; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
+            };
+            // the next output maps' weights and deltas are loaded while the
+            // current ones compute
+            load(aA, bA, 0);
+            for (int ks = 0; ks < C3 / 4; ks += 2) {
+                if (ks + 1 < C3 / 4) load(aB, bB, ks + 1);
+                compute(aA, bA);
+                if (ks + 1 < C3 / 4) {
+                    if (ks + 2 < C3 / 4) load(aA, bA, ks + 2);
+                    compute(aB, bB);
+                }
+            }
+            float *dst = sm.s2 + (4 * blk + lg) * NY2;
+            float *dm[3];
+            bool mv[3];
+#pragma unroll
+            for (int j = 0; j < 3; ++j) {
+                int m = 16 * j + lr;
+                mv[j] = m < M3;
+                dm[j] = dst + (mv[j] ? window_pos(m >> 2, m & 3, 3, H2) : 0);
+            }
+            // scatter grouped by kernel offset uv: inside a group the 3 x 64
+            // lanes write distinct addresses; wave_lds_order() orders the
+            // groups, whose targets overlap
+#pragma unroll
+            for (int i = 0; i < 9; ++i)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int uv = 4 * i + r, u = uv / 6, v = uv - 6 * u;
+#pragma unroll
+                    for (int j = 0; j < 3; ++j)
+                        if (mv[j]) dm[j][u * H2 + v] += acc[i][j][r];
+                    wave_lds_order();
+                }
+        }
+        __syncthreads();
+
+        // conv3 weight gradient G[o][k] = sum_m d3[o][m] y2col[m][k], pushed.
+        // Maps 0..95 on 32x32x2 tiles: element r of a tile holds maps
+        // 8(r/4) + r%4 and that + 4 at 32 consecutive k, so a push
+        // instruction writes two 128-byte runs of weights.  Maps 96..99 on
+        // the 16-block 4x4x1 instruction with block b, column c at
+        // k = 4b + c: element r holds map 96 + r at 64 consecutive k.
+        // Wavefront w takes the 64-column groups w, w + 4, ... (a column
+        // beyond KC3 computes values never pushed).
+        {
+            float a32[3][18];  // A[o = 32i + l%32][m = 2ms + l/32]
+#pragma unroll
+            for (int i = 0; i < 3; ++i)
+#pragma unroll
+                for (int ms = 0; ms < 18; ++ms)
+                    a32[i][ms] = sm.d3[(32 * i + (lane & 31)) * M3P + 2 * ms + (lane >> 5)];
+            const float *a4 = sm.d3 + (96 + (lane & 3)) * M3P;  // A[block][l%4][m]: map 96 + l%4
+            for (int grp = wave; grp < (KC3 / 16 + 3) / 4; grp += NW) {
+                f16 c32[3][2];
+                f4 c4[2];
+                const float *y32[2];
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+                    const int k = 64 * grp + 32 * kt + (lane & 31);
+                    y32[kt] = sm.y2 + (k < KC3 ? sm.koff3[k] : 0);
+                }
+                const int k4 = 64 * grp + lane;
+                const float *y4 = sm.y2 + (k4 < KC3 ? sm.koff3[k4] : 0);
+#pragma unroll
+                for (int ms = 0; ms < 18; ++ms) {
+                    const int m = 2 * ms + (lane >> 5), wp = window_pos(m >> 2, m & 3, 3, H2);
+                    float bv[2];
+#pragma unroll
+                    for (int kt = 0; kt < 2; ++kt) bv[kt] = y32[kt][wp];
+#pragma unroll
+                    for (int i = 0; i < 3; ++i)
+#pragma unroll
+                        for (int kt = 0; kt < 2; ++kt)
+                            c32[i][kt] = mfma32(a32[i][ms], bv[kt], ms == 0 ? f16{} : c32[i][kt]);
+                }
+                // two partial sums (even and odd m) keep the chain short
+#pragma unroll
+                for (int m = 0; m < M3; ++m) {
+                    const float bv = y4[window_pos(m >> 2, m & 3, 3, H2)];
+                    c4[m & 1] = mfma4(a4[m], bv, m < 2 ? f4{} : c4[m & 1]);
+                }
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+                    const int k = 64 * grp + 32 * kt + (lane & 31);
+                    if (k < KC3) {
+#pragma unroll
+                        for (int i = 0; i < 3; ++i)
+#pragma unroll
+                            for (int r = 0; r < 16; ++r) {
+                                const int o = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                                push(OW3 + o * KC3 + k, c32[i][kt][r]);
+                            }
+                    }
+                }
+                if (k4 < KC3) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) push(OW3 + (96 + r) * KC3 + k4, c4[0][r] + c4[1][r]);
+                }
+            }
+            if (tid < C3) {
+                // four partial sums over the window elements, then combined
+                float g4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int m = 0; m < M3; ++m) g4[m & 3] += sm.d3[tid * M3P + m];
+                push(OB3 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+            }
+        }
+        __syncthreads();
+
+        // conv2 deltas at the pooled positions (in place of y2); the delta of a
+        // conv2 output off its window's maximum is zero
+        for (int t = tid; t < C2 * NY2; t += NT) sm.y2[t] = sm.s2[t] * dact_from_y(sm.y2[t]);
+        __syncthreads();
+        // the conv1 output again (its region held the conv3 buffers meanwhile)
+        conv1_forward();
+        __syncthreads();
+
+        // conv2 weight gradient G[o][k] = sum_m d2[o][m] a1col[m][k], pushed:
+        // rows o (4 tiles), cols k = (c,u,v) (32 tiles, wavefront w takes
+        // w, w + 4, ...), K = the 484 outputs in (P, w) order, one pooled
+        // position per k-step; d2[o][(P, w)] is the pooled delta where w is
+        // the window's maximum and 0 elsewhere.
+        {
+            f4 acc[4][8];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int q = 0; q < 8; ++q) acc[i][q] = f4{0.f, 0.f, 0.f, 0.f};
+            int ko[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) ko[q] = sm.koff2[16 * (wave + NW * q) + lr];
+            int orow[4];
+            bool ovv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                ovv[i] = 16 * i + lr < C2;
+                orow[i] = (ovv[i] ? 16 * i + lr : 0) * NY2;
+            }
+            const int wy = lg >> 1, wx = lg & 1;
+            for (int P = 0; P < NY2; ++P) {
+                const int py = P / Q2, px = P - py * Q2;
+                const int base = (2 * py + wy) * H1 + 2 * px + wx;
+                float av[4], bv[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    av[i] = (ovv[i] && sm.am2[orow[i] + P] == lg) ? sm.y2[orow[i] + P] : 0.0f;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) bv[q] = sm.a1[base + ko[q]];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) acc[i][q] = mfma(av[i], bv[q], acc[i][q]);
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int k = 16 * (wave + NW * q) + lr;
+                if (k >= KC2) continue;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int o = 16 * i + 4 * lg + r;
+                        if (o < C2) push(OW2 + o * KC2 + k, acc[i][q][r]);
+                    }
+            }
+            if (tid < C2) {
+                float g4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+                for (int P = 0; P < NY2; ++P) g4[P & 3] += sm.y2[tid * NY2 + P];
+                push(OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+            }
+        }
+        __syncthreads();
+        // f'(conv1 output) in place; clear the conv1 error buffer
+        for (int t = tid; t < C1 * NA1; t += NT) {
+            sm.a1[t] = dact_from_y(sm.a1[t]);
+            sm.e1[t] = 0.0f;
+        }
+        __syncthreads();
+
+        // conv2 backward data: C[k][m] = sum_o W2[o][k] d2[o][m], k = (c,u,v),
+        // col2im into e1[c][pos(m) + (u,v)].  Input maps in blocks of 4, a
+        // block owned by one wavefront (wavefront 0 also takes block 4).  Row
+        // q of tile i holds map c0 + q/4 at uv = 4i + q%4 (7 tiles), so the
+        // four lane groups of an accumulator element hold four different maps
+        // at one (u,v): no scatter instruction has two lanes on one address,
+        // and wave_lds_order() keeps the overlapping groups in order.  The
+        // block's weights (15 k-steps x 7 tiles) stay in registers while its
+        // columns are computed four tiles at a time.
+        for (int blk = wave; blk < C1 / 4; blk += NW) {
+            const int c0 = 4 * blk;
+            float av[15][7];
+#pragma unroll
+            for (int ks = 0; ks < 15; ++ks) {
+                const float *w2 = W + OW2 + (4 * ks + lg) * KC2 + (c0 + (lr >> 2)) * 25 + (lr & 3);
+#pragma unroll
+                for (int i = 0; i < 7; ++i) av[ks][i] = (4 * i + (lr & 3) < 25) ? w2[4 * i] : 0.0f;
+            }
+            for (int j0 = 0; j0 < M2T; j0 += 4) {
+                f4 acc[7][4];
+#pragma unroll
+                for (int i = 0; i < 7; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+                // B: d2[o][m] for this lane's column m = 16(j0 + j) + lr
+                int pq[4], wq[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int m = 16 * (j0 + j) + lr;
+                    pq[j] = (m < M2) ? (m >> 2) : -1;
+                    wq[j] = m & 3;
+                }
+#pragma unroll
+                for (int ks = 0; ks < 15; ++ks) {
+                    const int o = 4 * ks + lg;
+                    float bv[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        bv[j] = (pq[j] >= 0 && sm.am2[o * NY2 + pq[j]] == wq[j]) ? sm.y2[o * NY2 + pq[j]]
+                                                                                 : 0.0f;
+#pragma unroll
+                    for (int i = 0; i < 7; ++i)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) acc[i][j] = mfma(av[ks][i], bv[j], acc[i][j]);
+                }
+                // scatter: element r of tile i is (u,v) = uv 4i + r of map
+                // c0 + lg; column m = 4P + w is conv2 output (2py + w/2, 2px + w%2)
+                float *dp[4];
+                bool mv[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int m = 16 * (j0 + j) + lr, P = m >> 2, w = m & 3;
+                    const int py = P / Q2, px = P - py * Q2;
+                    mv[j] = m < M2;
+                    dp[j] = sm.e1 + (c0 + lg) * NA1 + (mv[j] ? (2 * py + (w >> 1)) * H1 + 2 * px + (w & 1) : 0);
+                }
+#pragma unroll
+                for (int i = 0; i < 7; ++i)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int uv = 4 * i + r, u = uv / 5, v = uv - 5 * u;
+                        if (uv >= 25) continue;
+#pragma unroll
+                        for (int j = 0; j < 4; ++j)
+                            if (mv[j]) dp[j][u * H1 + v] += acc[i][j][r];
+                        wave_lds_order();
+                    }
+            }
+        }
+        __syncthreads();
+        // conv1 deltas
+        for (int t = tid; t < C1 * NA1; t += NT) sm.e1[t] *= sm.a1[t];
+        __syncthreads();
+
+        // conv1 weight gradient G[o][uv] = sum over the 676 outputs of the
+        // delta times the input under the kernel: rows o (2 tiles), cols
+        // uv = 4u + v, K = outputs (k-step ks covers outputs 4ks..4ks+3) split
+        // over the wavefronts, the partial tiles summed in wavefront order.
+        // Bias gradient: the deltas summed per map.
+        {
+            f4 acc[2][2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int t = 0; t < 2; ++t) acc[h][t] = f4{0.f, 0.f, 0.f, 0.f};
+            const int oa = lr, ob = (16 + lr < C1) ? 16 + lr : 0;
+            const bool vb = 16 + lr < C1;
+            const int xo = (lr >> 2) * IN + (lr & 3);
+            auto step = [&](int ks, f4 (&c)[2]) {
+                const int m = 4 * ks + lg, my = m / H1, mx = m - my * H1;
+                const float bx = sm.x[my * IN + mx + xo];
+                const float a0 = sm.e1[oa * NA1 + m];
+                const float a1v = vb ? sm.e1[ob * NA1 + m] : 0.0f;
+                c[0] = mfma(a0, bx, c[0]);
+                c[1] = mfma(a1v, bx, c[1]);
+            };
+            int ks = wave;
+            for (; ks + NW < NA1 / 4; ks += 2 * NW) {
+                step(ks, acc[0]);
+                step(ks + NW, acc[1]);
+            }
+            if (ks < NA1 / 4) step(ks, acc[0]);
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+                *(f4 *)(sm.red1 + ((wave * 2 + t) * 64 + lane) * 4) = acc[0][t] + acc[1][t];
+            __syncthreads();
+            for (int t = tid; t < C1 * 16 + C1; t += NT) {
+                if (t < C1 * 16) {
+                    const int o = t >> 4, uv = t & 15, tile = o >> 4, row = o & 15;
+                    const int e = ((row >> 2) * 16 + uv) * 4 + (row & 3);
+                    float g = sm.red1[(0 * 2 + tile) * 256 + e];
+#pragma unroll
+                    for (int w = 1; w < NW; ++w) g += sm.red1[(w * 2 + tile) * 256 + e];
+                    push(OW1 + t, g);
+                } else {
+                    const int o = t - C1 * 16;
+                    float g4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+                    for (int q = 0; q < NA1; ++q) g4[q & 3] += sm.e1[o * NA1 + q];
+                    push(OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
+} // namespace
+
+bool fused_t1_matches(const Net &net) {
+    static const int spec[][3] = {{kConv, 20, 4}, {kPool, 0, 1}, {kConv, 60, 5}, {kPool, 0, 2},
+                                  {kConv, 100, 6}, {kPool, 0, 2}, {kFc, 150, 0}, {kFc, 10, 0}};
+    if (net.n_layers != 8 || net.in_size != NX || net.n_params != NPARAM) return false;
+    for (int l = 0; l < 8; ++l) {
+        const Layer &ly = net.L[l];
+        if (ly.kind != spec[l][0]) return false;
+        if (ly.kind != kFc && ly.k != spec[l][2]) return false;
+        if (ly.kind != kPool && ly.cout != spec[l][1]) return false;
+    }
+    return net.L[0].hin == IN && net.L[0].win == IN;
+}
+
+hipError_t launch_fused_t1(int mode, const WorkArgs &a, int grid, hipStream_t s) {
+    switch (mode) {
+    case kTrainAtomic: fused_t1_kernel<kTrainAtomic><<<grid, NT, 0, s>>>(a); break;
+    case kTrainRacy: fused_t1_kernel<kTrainRacy><<<grid, NT, 0, s>>>(a); break;
+    case kForwardBackward: fused_t1_kernel<kForwardBackward><<<grid, NT, 0, s>>>(a); break;
+    case kEvaluate: fused_t1_kernel<kEvaluate><<<grid, NT, 0, s>>>(a); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+int fused_t1_blocks_per_cu() {
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fused_t1_kernel<kTrainAtomic>, NT, 0) !=
+        hipSuccess)
+        return 0;
+    return nb;
+}
+
+} // namespace chaos
