@@ -13,9 +13,10 @@ Prints one JSON line.  Extra fields:
                 MI355X FP32 peak
   cpu_baseline  the CPU oracle (sequential per-sample SGD, one core) on a
                 bounded sample of the same workload
-  rows          training throughput of the small and medium nets on the same
-                set (every resident worker, with the FP32-peak fraction and
-                the oracle's sequential rate on a short prefix), and the
+  rows          training throughput of the small and medium nets and of
+                Table I's large net on the same set (every resident worker,
+                with the FP32-peak fraction and the oracle's sequential rate
+                on a short prefix), and the
                 throughput of the frozen-weight 16,384-sample batch gradient
                 and of the 10,000-sample test forward pass of the large net
 """
@@ -322,7 +323,7 @@ def main():
     rows = None
     if not args.no_rows:
         rows = {}
-        for name in ("small", "medium"):
+        for name in ("small", "medium", "large_table1"):
             if name != args.net:
                 rows[f"train_{name}_{args.samples}"] = train_row(
                     chaos, wl, torch, name, xd, yd, x, y, args.steps,

@@ -12,7 +12,7 @@
 // in its epilogue.  LDS is reused across phases: region A holds the conv1
 // output in the forward pass, then the conv3 split-K partials, the conv3
 // backward buffers, the conv1 output again (recomputed for the conv2 weight
-// gradient, then turned into f'), and last the conv1 partial gradient tiles;
+// gradient and f'), and last the conv1 partial gradient tiles;
 // region B holds the pool2/FC1 values, then the conv1 output errors.
 #include <type_traits>
 
@@ -58,7 +58,7 @@ constexpr int M3 = 36, M3P = 48;                // padded to 3 tiles of 16
 struct alignas(16) Smem {
     float x[NX + 3];
     union {                              // region A
-        float a1[C1 * NA1];              // conv1 output; later f'(conv1 output)
+        float a1[C1 * NA1];              // conv1 output
         float red3[2 * 21 * 256];        // conv3 split-K partial sums (forward)
         struct {
             float s2[C2 * NY2];          // conv3 backward-data sums
@@ -182,7 +182,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         // wavefront w takes output maps 16w..16w+15 (one column tile) for all
         // rows; K = 500 (padded to 512) in super-steps of 16, lane group g
         // holding k = 16S + 4g + e at sub-step e, so its four weights of a
-        // super-step are one 16-byte load, requested two super-steps ahead.
+        // super-step are one 16-byte load, requested three super-steps ahead.
         {
             const int o = 16 * wave + lr;
             const bool ov = o < C2;
@@ -197,31 +197,47 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
             f4 acc[M2T];
 #pragma unroll
             for (int i = 0; i < M2T; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
+            // weights: unconditional 16-byte loads (the address is in bounds
+            // for every lane), zeroed by a select where the lane's k or map is
+            // past the end, so no branch separates a load from its use
             auto load = [&](int S) {
-                return (ov && 16 * S + 4 * lg < KC2) ? *(const f4 *)(wrow + 16 * S)
-                                                     : f4{0.f, 0.f, 0.f, 0.f};
+                const f4 v = *(const f4 *)(wrow + 16 * S);
+                const bool ok = ov && 16 * S + 4 * lg < KC2;
+                return f4{ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f};
             };
-            auto compute = [&](f4 b, int S) {
+            // A operands of sub-step (S, e) for every row tile; the next
+            // sub-step's are read while this one's matrix instructions run
+            float aC[M2T], aN[M2T];
+            auto read_a = [&](float (&av)[M2T], int off) {
+#pragma unroll
+                for (int i = 0; i < M2T; ++i) av[i] = sm.a1[base[i] + off];
+            };
+            auto step = [&](f4 b, int S) {
                 const int4 ko = *(const int4 *)(sm.koff2 + 16 * S + 4 * lg);
-                const int offs[4] = {ko.x, ko.y, ko.z, ko.w};
+                const int4 kn = *(const int4 *)(sm.koff2 + 16 * (S + 1 < KC2P / 16 ? S + 1 : S) + 4 * lg);
+                const int offs[5] = {ko.x, ko.y, ko.z, ko.w, kn.x};
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
+                for (int e = 0; e < 4; ++e) {
+                    read_a(aN, offs[e + 1]);
 #pragma unroll
-                    for (int i = 0; i < M2T; ++i) acc[i] = mfma(sm.a1[base[i] + offs[e]], b[e], acc[i]);
+                    for (int i = 0; i < M2T; ++i) acc[i] = mfma(aC[i], b[e], acc[i]);
+#pragma unroll
+                    for (int i = 0; i < M2T; ++i) aC[i] = aN[i];
+                }
             };
-            constexpr int NS = KC2P / 16;  // 32
-            f4 bA = load(0), bB = load(1), bC;
-            for (int S = 0; S < NS; S += 3) {
-                if (S + 2 < NS) bC = load(S + 2);
-                compute(bA, S);
-                if (S + 1 < NS) {
-                    if (S + 3 < NS) bA = load(S + 3);
-                    compute(bB, S + 1);
-                }
-                if (S + 2 < NS) {
-                    if (S + 4 < NS) bB = load(S + 4);
-                    compute(bC, S + 2);
-                }
+            constexpr int NS = KC2P / 16;  // 32 super-steps, a ring of four weight buffers
+            static_assert(NS % 4 == 0, "whole rounds");
+            f4 b0 = load(0), b1 = load(1), b2 = load(2), b3;
+            read_a(aC, sm.koff2[4 * lg]);
+            for (int S = 0; S < NS; S += 4) {
+                b3 = load(S + 3);
+                step(b0, S);
+                b0 = load(S + 4 < NS ? S + 4 : NS - 1);
+                step(b1, S + 1);
+                b1 = load(S + 5 < NS ? S + 5 : NS - 1);
+                step(b2, S + 2);
+                b2 = load(S + 6 < NS ? S + 6 : NS - 1);
+                step(b3, S + 3);
             }
             if (ov) {
                 const float bias = W[OB2 + o];
@@ -732,86 +748,31 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         __syncthreads();
 
         // conv2 deltas at the pooled positions (in place of y2); the delta of a
-        // conv2 output off its window's maximum is zero
+        // conv2 output off its window's maximum is zero.  Clear the conv1
+        // error buffer.
         for (int t = tid; t < C2 * NY2; t += NT) sm.y2[t] = sm.s2[t] * dact_from_y(sm.y2[t]);
+        for (int t = tid; t < C1 * NA1; t += NT) sm.e1[t] = 0.0f;
         __syncthreads();
         // the conv1 output again (its region held the conv3 buffers meanwhile)
         conv1_forward();
         __syncthreads();
 
-        // conv2 weight gradient G[o][k] = sum_m d2[o][m] a1col[m][k], pushed:
-        // rows o (4 tiles), cols k = (c,u,v) (32 tiles, wavefront w takes
-        // w, w + 4, ...), K = the 484 outputs in (P, w) order, one pooled
-        // position per k-step; d2[o][(P, w)] is the pooled delta where w is
-        // the window's maximum and 0 elsewhere.
-        {
-            f4 acc[4][8];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int q = 0; q < 8; ++q) acc[i][q] = f4{0.f, 0.f, 0.f, 0.f};
-            int ko[8];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) ko[q] = sm.koff2[16 * (wave + NW * q) + lr];
-            int orow[4];
-            bool ovv[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                ovv[i] = 16 * i + lr < C2;
-                orow[i] = (ovv[i] ? 16 * i + lr : 0) * NY2;
-            }
-            const int wy = lg >> 1, wx = lg & 1;
-            for (int P = 0; P < NY2; ++P) {
-                const int py = P / Q2, px = P - py * Q2;
-                const int base = (2 * py + wy) * H1 + 2 * px + wx;
-                float av[4], bv[8];
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    av[i] = (ovv[i] && sm.am2[orow[i] + P] == lg) ? sm.y2[orow[i] + P] : 0.0f;
-#pragma unroll
-                for (int q = 0; q < 8; ++q) bv[q] = sm.a1[base + ko[q]];
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int q = 0; q < 8; ++q) acc[i][q] = mfma(av[i], bv[q], acc[i][q]);
-            }
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const int k = 16 * (wave + NW * q) + lr;
-                if (k >= KC2) continue;
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const int o = 16 * i + 4 * lg + r;
-                        if (o < C2) push(OW2 + o * KC2 + k, acc[i][q][r]);
-                    }
-            }
-            if (tid < C2) {
-                float g4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-                for (int P = 0; P < NY2; ++P) g4[P & 3] += sm.y2[tid * NY2 + P];
-                push(OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
-            }
-        }
-        __syncthreads();
-        // f'(conv1 output) in place; clear the conv1 error buffer
-        for (int t = tid; t < C1 * NA1; t += NT) {
-            sm.a1[t] = dact_from_y(sm.a1[t]);
-            sm.e1[t] = 0.0f;
-        }
-        __syncthreads();
-
-        // conv2 backward data: C[k][m] = sum_o W2[o][k] d2[o][m], k = (c,u,v),
-        // col2im into e1[c][pos(m) + (u,v)].  Input maps in blocks of 4, a
-        // block owned by one wavefront (wavefront 0 also takes block 4).  Row
-        // q of tile i holds map c0 + q/4 at uv = 4i + q%4 (7 tiles), so the
-        // four lane groups of an accumulator element hold four different maps
-        // at one (u,v): no scatter instruction has two lanes on one address,
-        // and wave_lds_order() keeps the overlapping groups in order.  The
-        // block's weights (15 k-steps x 7 tiles) stay in registers while its
-        // columns are computed four tiles at a time.
-        for (int blk = wave; blk < C1 / 4; blk += NW) {
+        // conv2 backward data and conv2 weight gradient, which read the same
+        // inputs and write different outputs, in one phase so that the work
+        // can be balanced over the wavefronts: backward data comes in 5 blocks
+        // of 4 input maps (wavefront w takes block w, wavefront 0 also block
+        // 4), the weight gradient in 32 column tiles (wavefront 0 takes 3,
+        // the others 10, 10 and 9).
+        //
+        // Backward data: C[k][m] = sum_o W2[o][k] d2[o][m], k = (c,u,v),
+        // col2im into e1[c][pos(m) + (u,v)].  Row q of tile i holds map
+        // c0 + q/4 at uv = 4i + q%4 (7 tiles), so the four lane groups of an
+        // accumulator element hold four different maps at one (u,v): no
+        // scatter instruction has two lanes on one address, and
+        // wave_lds_order() keeps the overlapping groups in order.  A block's
+        // weights (15 k-steps x 7 tiles) stay in registers while its columns
+        // are computed four tiles at a time.
+        auto bwd_block = [&](int blk) {
             const int c0 = 4 * blk;
             float av[15][7];
 #pragma unroll
@@ -834,19 +795,21 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     pq[j] = (m < M2) ? (m >> 2) : -1;
                     wq[j] = m & 3;
                 }
+                float bv[15][4];
 #pragma unroll
                 for (int ks = 0; ks < 15; ++ks) {
                     const int o = 4 * ks + lg;
-                    float bv[4];
 #pragma unroll
                     for (int j = 0; j < 4; ++j)
-                        bv[j] = (pq[j] >= 0 && sm.am2[o * NY2 + pq[j]] == wq[j]) ? sm.y2[o * NY2 + pq[j]]
-                                                                                 : 0.0f;
+                        bv[ks][j] = (pq[j] >= 0 && sm.am2[o * NY2 + pq[j]] == wq[j])
+                                        ? sm.y2[o * NY2 + pq[j]] : 0.0f;
+                }
+#pragma unroll
+                for (int ks = 0; ks < 15; ++ks)
 #pragma unroll
                     for (int i = 0; i < 7; ++i)
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) acc[i][j] = mfma(av[ks][i], bv[j], acc[i][j]);
-                }
+                        for (int j = 0; j < 4; ++j) acc[i][j] = mfma(av[ks][i], bv[ks][j], acc[i][j]);
                 // scatter: element r of tile i is (u,v) = uv 4i + r of map
                 // c0 + lg; column m = 4P + w is conv2 output (2py + w/2, 2px + w%2)
                 float *dp[4];
@@ -870,10 +833,85 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                         wave_lds_order();
                     }
             }
+        };
+        // Weight gradient G[o][k] = sum_m d2[o][m] a1col[m][k], pushed: rows o
+        // (4 tiles), four column tiles of k = (c,u,v) per pass, K = the 484
+        // outputs in (P, w) order, one pooled position per k-step;
+        // d2[o][(P, w)] is the pooled delta where w is the window's maximum
+        // and 0 elsewhere.
+        auto wgrad_tiles = [&](int jt0, int nt) {
+            f4 acc[4][4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) acc[i][q] = f4{0.f, 0.f, 0.f, 0.f};
+            int ko[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) ko[q] = (q < nt) ? sm.koff2[16 * (jt0 + q) + lr] : 0;
+            int orow[4];
+            bool ovv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                ovv[i] = 16 * i + lr < C2;
+                orow[i] = (ovv[i] ? 16 * i + lr : 0) * NY2;
+            }
+            const int wy = lg >> 1, wx = lg & 1;
+            // operands of pooled position P (read one position ahead)
+            auto operands = [&](int P, float (&av)[4], float (&bv)[4]) {
+                const int py = P / Q2, px = P - py * Q2;
+                const int base = (2 * py + wy) * H1 + 2 * px + wx;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    av[i] = (ovv[i] && sm.am2[orow[i] + P] == lg) ? sm.y2[orow[i] + P] : 0.0f;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) bv[q] = sm.a1[base + ko[q]];
+            };
+            auto compute = [&](const float (&av)[4], const float (&bv)[4]) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) acc[i][q] = mfma(av[i], bv[q], acc[i][q]);
+            };
+            float aA[4], bA[4], aB[4], bB[4];
+            operands(0, aA, bA);
+            for (int P = 0; P < NY2; P += 2) {
+                if (P + 1 < NY2) operands(P + 1, aB, bB);
+                compute(aA, bA);
+                if (P + 1 < NY2) {
+                    if (P + 2 < NY2) operands(P + 2, aA, bA);
+                    compute(aB, bB);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int k = 16 * (jt0 + q) + lr;
+                if (q >= nt || k >= KC2) continue;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int o = 16 * i + 4 * lg + r;
+                        if (o < C2) push(OW2 + o * KC2 + k, acc[i][q][r]);
+                    }
+            }
+        };
+        {
+            bwd_block(wave);
+            if (wave == 0) bwd_block(4);
+            // column tiles [t0, t1) of this wavefront
+            const int t0 = (wave == 0) ? 0 : 3 + 10 * (wave - 1);
+            const int t1 = (wave == 0) ? 3 : (wave == 3 ? 32 : t0 + 10);
+            for (int jt = t0; jt < t1; jt += 4) wgrad_tiles(jt, (t1 - jt < 4) ? t1 - jt : 4);
+            if (tid < C2) {
+                float g4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+                for (int P = 0; P < NY2; ++P) g4[P & 3] += sm.y2[tid * NY2 + P];
+                push(OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+            }
         }
         __syncthreads();
-        // conv1 deltas
-        for (int t = tid; t < C1 * NA1; t += NT) sm.e1[t] *= sm.a1[t];
+        // conv1 deltas: e1 * f'(conv1 output)
+        for (int t = tid; t < C1 * NA1; t += NT) sm.e1[t] *= dact_from_y(sm.a1[t]);
         __syncthreads();
 
         // conv1 weight gradient G[o][uv] = sum over the 676 outputs of the
