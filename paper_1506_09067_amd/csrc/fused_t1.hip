@@ -775,11 +775,17 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         auto bwd_block = [&](int blk) {
             const int c0 = 4 * blk;
             float av[15][7];
+            // (loads are unconditional, from a clamped address, and zeroed by
+            // a select: no branch between a load and its use)
 #pragma unroll
             for (int ks = 0; ks < 15; ++ks) {
                 const float *w2 = W + OW2 + (4 * ks + lg) * KC2 + (c0 + (lr >> 2)) * 25 + (lr & 3);
 #pragma unroll
-                for (int i = 0; i < 7; ++i) av[ks][i] = (4 * i + (lr & 3) < 25) ? w2[4 * i] : 0.0f;
+                for (int i = 0; i < 7; ++i) {
+                    const bool ok = 4 * i + (lr & 3) < 25;
+                    const float v = w2[ok ? 4 * i : 0];
+                    av[ks][i] = ok ? v : 0.0f;
+                }
             }
             for (int j0 = 0; j0 < M2T; j0 += 4) {
                 f4 acc[7][4];
@@ -800,9 +806,12 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 for (int ks = 0; ks < 15; ++ks) {
                     const int o = 4 * ks + lg;
 #pragma unroll
-                    for (int j = 0; j < 4; ++j)
-                        bv[ks][j] = (pq[j] >= 0 && sm.am2[o * NY2 + pq[j]] == wq[j])
-                                        ? sm.y2[o * NY2 + pq[j]] : 0.0f;
+                    for (int j = 0; j < 4; ++j) {
+                        const int q = o * NY2 + (pq[j] >= 0 ? pq[j] : 0);
+                        const int am = sm.am2[q];
+                        const float v = sm.y2[q];
+                        bv[ks][j] = (pq[j] >= 0 && am == wq[j]) ? v : 0.0f;
+                    }
                 }
 #pragma unroll
                 for (int ks = 0; ks < 15; ++ks)
@@ -861,8 +870,11 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 const int py = P / Q2, px = P - py * Q2;
                 const int base = (2 * py + wy) * H1 + 2 * px + wx;
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    av[i] = (ovv[i] && sm.am2[orow[i] + P] == lg) ? sm.y2[orow[i] + P] : 0.0f;
+                for (int i = 0; i < 4; ++i) {
+                    const int am = sm.am2[orow[i] + P];
+                    const float v = sm.y2[orow[i] + P];
+                    av[i] = (ovv[i] && am == lg) ? v : 0.0f;
+                }
 #pragma unroll
                 for (int q = 0; q < 4; ++q) bv[q] = sm.a1[base + ko[q]];
             };
