@@ -133,16 +133,21 @@ __device__ __forceinline__ float dact_from_y(float y) {
     return (kActB / kActA) * (kActA * kActA - y * y);
 }
 
-// Max over a 2x2 window held in one lane's accumulator (window elements in
-// row-major order); the first maximum wins.
+// Max over a 2x2 window of activated conv outputs held in one lane's
+// accumulator (window elements in row-major order; the first maximum wins).
+// The activation is strictly increasing, so the maximum of f(z) is f of the
+// maximum of z: the window is compared on z and f is evaluated once.  (Where
+// f would round two different z to the same fp32 value, the larger z wins,
+// which is the maximum of the exact f.)
 __device__ __forceinline__ void pool4(f4 acc, float bias, float &ymax, int &arg) {
-    ymax = act_y(acc[0] + bias);
+    float zmax = acc[0] + bias;
     arg = 0;
 #pragma unroll
     for (int r = 1; r < 4; ++r) {
-        float y = act_y(acc[r] + bias);
-        if (y > ymax) { ymax = y; arg = r; }
+        float z = acc[r] + bias;
+        if (z > zmax) { zmax = z; arg = r; }
     }
+    ymax = act_y(zmax);
 }
 
 // position (row-major index into a map of width `wd`) of element w of the

@@ -52,7 +52,7 @@ struct alignas(16) SmemCpcp {
     float x[S::NX + 3];
     float p1[S::C1 * S::NP1];            // pool1 output, later pool1 errors/deltas in e1
     float e1[S::C1 * S::NP1];            // dE/d(pool1 output)
-    float y2[S::C2 * S::NY2];            // conv2 output
+    float y2[S::C2 * S::NY2];            // conv2 output before the activation
     alignas(16) float d2[S::C2P * 96];   // conv2 output deltas (dense, zero off the argmax);
                                          // conv2 forward partial sums before that
     alignas(16) float p2[S::NF1];        // pool2 output
@@ -257,7 +257,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             int pe = 16 * (rt0 + i) + 4 * lg + r;
-                            if (pe < S::NY2) sm.y2[o * S::NY2 + pe] = act_y(t[r] + bias);
+                            if (pe < S::NY2) sm.y2[o * S::NY2 + pe] = t[r] + bias;
                         }
                     }
                 }
@@ -265,19 +265,22 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         }
         __syncthreads();
 
-        // ---- pool2: 3x3 windows of the 9x9 maps, first maximum wins ----
+        // ---- pool2: 3x3 windows of the 9x9 maps, first maximum wins.  y2
+        //      holds the conv2 outputs before the activation; f is strictly
+        //      increasing, so the window's maximum is taken on z and f is
+        //      applied to it alone. ----
         for (int t = tid; t < S::NF1; t += NT) {
             int o = t / S::NP2, P = t - o * S::NP2;
             int py = P / 3, px = P - 3 * py;
-            const float *yo = sm.y2 + o * S::NY2 + 3 * py * S::H2 + 3 * px;
-            float m = yo[0];
+            const float *zo = sm.y2 + o * S::NY2 + 3 * py * S::H2 + 3 * px;
+            float m = zo[0];
             int ag = 0;
 #pragma unroll
             for (int w = 1; w < 9; ++w) {
-                float v = yo[(w / 3) * S::H2 + (w % 3)];
+                float v = zo[(w / 3) * S::H2 + (w % 3)];
                 if (v > m) { m = v; ag = w; }
             }
-            sm.p2[t] = m;
+            sm.p2[t] = act_y(m);
             sm.am2[t] = (unsigned char)ag;
         }
         __syncthreads();
@@ -501,19 +504,32 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 xv[c] = (i < S::NF1) ? sm.p2[i] : 0.0f;
                 ep[c] = 0.0f;
             }
-            for (int j = wave; j < S::F1; j += 2 * NW) {
-                const int j2 = j + NW;
-                const float d = sm.dh[j], d2 = (j2 < S::F1) ? sm.dh[j2] : 0.0f;
-                float old[2][IC];
+            // R rows per step: IC * R returning pushes in flight before their
+            // returns are used (a wavefront's rows are still summed in
+            // increasing order)
+            constexpr int R = (64 / IC < 16) ? 64 / IC : 16;
+            for (int j = wave; j < S::F1; j += R * NW) {
+                float old[R][IC], dr[R];
 #pragma unroll
-                for (int c = 0; c < IC; ++c) {
-                    int i = lane + 64 * c;
-                    old[0][c] = (i < S::NF1) ? push.with_old(S::OF1 + j * S::NF1 + i, d * xv[c]) : 0.0f;
-                    old[1][c] = (i < S::NF1 && j2 < S::F1)
-                                    ? push.with_old(S::OF1 + j2 * S::NF1 + i, d2 * xv[c]) : 0.0f;
+                for (int r = 0; r < R; ++r) {
+                    const int jr = j + r * NW;
+                    dr[r] = (jr < S::F1) ? sm.dh[jr] : 0.0f;
+                    if (jr < S::F1) {
+#pragma unroll
+                        for (int c = 0; c < IC; ++c) {
+                            int i = lane + 64 * c;
+                            old[r][c] = (i < S::NF1) ? push.with_old(S::OF1 + jr * S::NF1 + i, dr[r] * xv[c])
+                                                     : 0.0f;
+                        }
+                    } else {
+#pragma unroll
+                        for (int c = 0; c < IC; ++c) old[r][c] = 0.0f;
+                    }
                 }
 #pragma unroll
-                for (int c = 0; c < IC; ++c) ep[c] = fmaf(old[1][c], d2, fmaf(old[0][c], d, ep[c]));
+                for (int r = 0; r < R; ++r)
+#pragma unroll
+                    for (int c = 0; c < IC; ++c) ep[c] = fmaf(old[r][c], dr[r], ep[c]);
             }
 #pragma unroll
             for (int c = 0; c < IC; ++c) {

@@ -51,6 +51,7 @@ static_assert(OW2 % 4 == 0 && KC2 % 4 == 0 && OF1 % 4 == 0 && OW3 % 4 == 0 && KC
 
 constexpr int NT = 256;   // threads per worker
 constexpr int NW = NT / 64;
+constexpr int FC1_ROWS = 4;  // FC1 rows a wavefront pushes per step (returning adds)
 
 // conv3 output rows m = 4 * P + w (P pooled 3x3 position, w window element)
 constexpr int M3 = 36, M3P = 48;                // padded to 3 tiles of 16
@@ -556,28 +557,31 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     xv[c] = (i < NF1) ? sm.p3[i] : 0.0f;
                     ep[c] = 0.0f;
                 }
-                // two rows per step: 30 pushes in flight before their returns are used
-                for (int j = wave; j < F1; j += 2 * NW) {
-                    const int j2 = j + NW;
-                    const float d = sm.dh[j], d2 = (j2 < F1) ? sm.dh[j2] : 0.0f;
-                    float old[2][15];
+                // FC1_ROWS rows per step: 15 FC1_ROWS pushes in flight before
+                // their returns are used (a wavefront's rows are still summed
+                // in increasing order)
+                for (int j = wave; j < F1; j += FC1_ROWS * NW) {
+                    float old[FC1_ROWS][15], dr[FC1_ROWS];
 #pragma unroll
-                    for (int c = 0; c < 15; ++c) {
-                        int i = lane + 64 * c;
-                        old[0][c] = (i < NF1) ? push.with_old(OF1 + j * NF1 + i, d * xv[c]) : 0.0f;
-                    }
-                    if (j2 < F1) {
+                    for (int r = 0; r < FC1_ROWS; ++r) {
+                        const int jr = j + r * NW;
+                        dr[r] = (jr < F1) ? sm.dh[jr] : 0.0f;
+                        if (jr < F1) {
 #pragma unroll
-                        for (int c = 0; c < 15; ++c) {
-                            int i = lane + 64 * c;
-                            old[1][c] = (i < NF1) ? push.with_old(OF1 + j2 * NF1 + i, d2 * xv[c]) : 0.0f;
+                            for (int c = 0; c < 15; ++c) {
+                                int i = lane + 64 * c;
+                                old[r][c] = (i < NF1) ? push.with_old(OF1 + jr * NF1 + i, dr[r] * xv[c])
+                                                      : 0.0f;
+                            }
+                        } else {
+#pragma unroll
+                            for (int c = 0; c < 15; ++c) old[r][c] = 0.0f;
                         }
-                    } else {
-#pragma unroll
-                        for (int c = 0; c < 15; ++c) old[1][c] = 0.0f;
                     }
 #pragma unroll
-                    for (int c = 0; c < 15; ++c) ep[c] = fmaf(old[1][c], d2, fmaf(old[0][c], d, ep[c]));
+                    for (int r = 0; r < FC1_ROWS; ++r)
+#pragma unroll
+                        for (int c = 0; c < 15; ++c) ep[c] = fmaf(old[r][c], dr[r], ep[c]);
                 }
                 float *part = sm.fcpart;  // [wavefront][input]
 #pragma unroll
