@@ -42,6 +42,12 @@ struct Cpcp {
     static constexpr int NPARAM = OBF2 + F2;
     // FC1 rows read with 16-byte loads when every row start is 16-byte aligned
     static constexpr int FC1_VEC = (OF1 % 4 == 0 && NF1 % 4 == 0) ? 4 : 1;
+    // A weight vector of at most 8K floats (the small net: 25.6 KB) is copied
+    // into LDS once per sample and every later weight read of the sample is
+    // served from there: one round trip to memory per sample instead of one
+    // per layer and pass.
+    static constexpr bool STAGE = NPARAM <= 8192;
+    static constexpr int NPARAM4 = (NPARAM + 3) / 4 * 4;
 };
 
 constexpr int NT = 256, NW = 4;
@@ -62,14 +68,21 @@ struct alignas(16) SmemCpcp {
     alignas(16) int koff2[4 * S::KQ2];   // im2col offset into p1 of k = (c,u,v) (0 past KC2)
     unsigned char am1[S::C1 * S::NP1 + 16];
     unsigned char am2[S::NF1 + 16];
+    alignas(16) float w[S::STAGE ? S::NPARAM4 : 4];  // the weights read at the start of the sample
     int64_t idx;
 };
 
 template <class S, int MODE, int MINB>
 __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
     __shared__ SmemCpcp<S> sm;
-    const float *W = a.params;
+    const float *Wg = a.params;
+    // every weight read below goes through W: the LDS copy or the shared vector
+    const float *W = S::STAGE ? (const float *)sm.w : Wg;
     constexpr bool kTrain = (MODE == kTrainAtomic || MODE == kTrainRacy);
+    // the FC1 partial derivatives come from a separate read of the weights
+    // (frozen weights, or the LDS copy) instead of the values returned by the
+    // FC1 pushes
+    constexpr bool kFc1Read = (MODE == kForwardBackward) || S::STAGE;
 
     for (int k = threadIdx.x; k < 4 * S::KQ2; k += NT) {
         int c = k / 25, uv = k - 25 * c, u = uv / 5, v = uv - 5 * u;
@@ -99,7 +112,27 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             if (a.claims && tid == 0) atomicAdd(a.claims + idx, 1);
         }
         const int label = a.labels[idx];
-        for (int i = tid; i < S::NX; i += NT) sm.x[i] = a.x[idx * S::NX + i];
+        if constexpr (S::STAGE) {
+            // the weights of this sample: all 16-byte loads are issued before
+            // the first LDS write (the vector starts 16-byte aligned)
+            constexpr int N4 = S::NPARAM / 4, PER = (N4 + NT - 1) / NT, TAIL = S::NPARAM - 4 * N4;
+            f4 wv[PER];
+#pragma unroll
+            for (int q = 0; q < PER; ++q) {
+                const int t4 = tid + NT * q;
+                wv[q] = (t4 < N4) ? *(const f4 *)(Wg + 4 * t4) : f4{0.f, 0.f, 0.f, 0.f};
+            }
+            const float wt = (tid < TAIL) ? Wg[4 * N4 + tid] : 0.0f;
+            for (int i = tid; i < S::NX; i += NT) sm.x[i] = a.x[idx * S::NX + i];
+#pragma unroll
+            for (int q = 0; q < PER; ++q) {
+                const int t4 = tid + NT * q;
+                if (t4 < N4) *(f4 *)(sm.w + 4 * t4) = wv[q];
+            }
+            if (tid < TAIL) sm.w[4 * N4 + tid] = wt;
+        } else {
+            for (int i = tid; i < S::NX; i += NT) sm.x[i] = a.x[idx * S::NX + i];
+        }
         __syncthreads();
 
         // ---- conv1 + pool1: rows (P, w) P < 169, cols o < C1, K = 16 ----
@@ -412,8 +445,8 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             push(S::OF2 + t, sm.dout[j] * sm.h[i]);
         }
         if (tid < S::F2) push(S::OBF2 + tid, sm.dout[tid]);
-        if constexpr (MODE == kForwardBackward) {
-            // frozen weights: read them, then push
+        if constexpr (kFc1Read) {
+            // read the weights (frozen, or this sample's LDS copy), then push
             // FC1 backward data (pre-update weights), summed over the rows in
             // row order: thread t owns VEC inputs (one 16-byte load per row when
             // aligned); with 16-byte loads the rows are split in two halves whose
@@ -549,7 +582,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 int w = (py % 3) * 3 + px % 3;
                 if (sm.am2[q] == w) {
                     float e;
-                    if constexpr (MODE == kForwardBackward)
+                    if constexpr (kFc1Read)
                         e = (S::FC1_VEC == 4) ? sm.e2[q] + sm.e2b[q] : sm.e2[q];
                     else
                         e = ((sm.y2[q] + sm.y2[S::NF1 + q]) + sm.y2[2 * S::NF1 + q]) + sm.y2[3 * S::NF1 + q];
@@ -845,6 +878,9 @@ int cpcp_blocks_per_cu() {
 }
 
 constexpr int kSmallMinBlocks = 3, kMediumMinBlocks = 2;
+static_assert(sizeof(SmemCpcp<Small>) * kSmallMinBlocks <= 160 * 1024 &&
+                  sizeof(SmemCpcp<Medium>) * kMediumMinBlocks <= 160 * 1024,
+              "resident workers per CU fit in the LDS");
 
 bool matches(const Net &net, int c1, int c2, int f1) {
     const int spec[6][3] = {{kConv, c1, 4}, {kPool, 0, 2}, {kConv, c2, 5},
