@@ -30,10 +30,11 @@ __device__ __forceinline__ float wave_sum(float v) {
 // Where a layer's weight gradient g goes (per element, once per sample):
 //   training   W[off] += -lr * g, an atomic fp32 add or a racy load/add/store
 //   frozen     each[off] = g (per-sample row) and/or part[off] += g, an atomic
-//              add into this worker's own zero-initialised row.  A worker's
-//              samples are separated by barriers that wait for its memory
-//              operations, so the adds into a row happen in sample order and
-//              the partial sums are reproducible bit for bit.
+//              add into this worker's own zero-initialised row.  Every
+//              wavefront of a worker waits for its memory operations before
+//              the worker starts its next sample, so the adds into a row
+//              happen in sample order and the partial sums are reproducible
+//              bit for bit.
 struct Push {
     int mode;
     float *params;
@@ -89,6 +90,16 @@ struct Push {
 // as weight pushes.
 __device__ __forceinline__ void wave_lds_order() {
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+}
+
+// Waits until every vector memory operation this wavefront has issued has
+// completed (s_waitcnt vmcnt(0)), its fire-and-forget weight pushes
+// included.  Workgroup barriers do not wait for them, so a worker that must
+// see its own updates (the next sample's weight reads; the next sample's adds
+// into a partial-sum row) has every wavefront wait here first.
+__device__ __forceinline__ void wait_vector_memory() {
+    // simm16: vmcnt 0, expcnt 7, lgkmcnt 15 (no wait on those two)
+    __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
 // Workgroup barrier that orders LDS only: the wavefronts' outstanding global

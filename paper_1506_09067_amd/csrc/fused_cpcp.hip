@@ -98,12 +98,13 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 
         if (tid == 0) sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1)
                                       : (int64_t)blockIdx.x + step * gridDim.x;
-        // Reads are on demand: before any weight of this sample is read, one
-        // wavefront drops the weights this CU and its L2 hold from earlier
-        // samples (an agent-scope acquire: the caches are shared by the
-        // workgroup, and the barrier below orders every wavefront's reads
-        // after it).  The previous sample's barriers waited for all of this
-        // worker's pushes.
+        // Reads are on demand.  Every wavefront first waits for its own
+        // pushes of the previous sample to complete (the worker sees its own
+        // updates: one worker is exact per-sample SGD); then one wavefront
+        // drops the weights this CU and its L2 hold from earlier samples (an
+        // agent-scope acquire: the caches are shared by the workgroup, and
+        // the barrier below orders every wavefront's reads after it).
+        wait_vector_memory();
         if (kTrain && wave == 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         __syncthreads();
         const int64_t idx = sm.idx;

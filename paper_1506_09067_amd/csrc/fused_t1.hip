@@ -111,10 +111,13 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         // ---- claim a sample (Section III-A.1) ----
         if (tid == 0) sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1)
                                       : (int64_t)blockIdx.x + step * gridDim.x;
-        // Reads are on demand: one wavefront drops the weights this CU and its
-        // L2 hold from earlier samples before any weight of this sample is read
-        // (the barrier orders every wavefront's reads after it); the previous
-        // sample's last barrier waited for all of this worker's pushes.
+        // Reads are on demand.  Every wavefront first waits for its own
+        // pushes of the previous sample to complete (the worker sees its own
+        // updates: one worker is exact per-sample SGD); then one wavefront
+        // drops the weights this CU and its L2 hold from earlier samples (an
+        // agent-scope acquire: the caches are shared by the workgroup, and
+        // the barrier below orders every wavefront's reads after it).
+        wait_vector_memory();
         if (kTrain && wave == 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         __syncthreads();
         const int64_t idx = sm.idx;
