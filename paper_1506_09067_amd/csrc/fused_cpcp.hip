@@ -48,6 +48,11 @@ struct Cpcp {
     // per layer and pass.
     static constexpr bool STAGE = NPARAM <= 8192;
     static constexpr int NPARAM4 = (NPARAM + 3) / 4 * 4;
+    // Otherwise the conv2 weights (80 KB for the medium net), read by the
+    // conv2 forward pass and again by its backward-data pass, are copied into
+    // LDS once per sample (one worker per CU then fits).
+    static constexpr int NW2 = C2 * KC2;
+    static constexpr bool STAGE2 = !STAGE && NW2 <= 20480 && OW2 % 4 == 0;
 };
 
 constexpr int NT = 256, NW = 4;
@@ -69,6 +74,7 @@ struct alignas(16) SmemCpcp {
     unsigned char am1[S::C1 * S::NP1 + 16];
     unsigned char am2[S::NF1 + 16];
     alignas(16) float w[S::STAGE ? S::NPARAM4 : 4];  // the weights read at the start of the sample
+    alignas(16) float w2[S::STAGE2 ? S::NW2 : 4];    // the conv2 weights read at the start of the sample
     int64_t idx;
 };
 
@@ -78,6 +84,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
     const float *Wg = a.params;
     // every weight read below goes through W: the LDS copy or the shared vector
     const float *W = S::STAGE ? (const float *)sm.w : Wg;
+    const float *W2 = S::STAGE2 ? (const float *)sm.w2 : W + S::OW2;  // conv2 weights [o][k]
     constexpr bool kTrain = (MODE == kTrainAtomic || MODE == kTrainRacy);
     // the FC1 partial derivatives come from a separate read of the weights
     // (frozen weights, or the LDS copy) instead of the values returned by the
@@ -131,6 +138,21 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 if (t4 < N4) *(f4 *)(sm.w + 4 * t4) = wv[q];
             }
             if (tid < TAIL) sm.w[4 * N4 + tid] = wt;
+        } else if constexpr (S::STAGE2) {
+            constexpr int N4 = S::NW2 / 4, PER = (N4 + NT - 1) / NT;
+            static_assert(S::NW2 % 4 == 0, "whole 16-byte loads");
+            f4 wv[PER];
+#pragma unroll
+            for (int q = 0; q < PER; ++q) {
+                const int t4 = tid + NT * q;
+                wv[q] = (t4 < N4) ? *(const f4 *)(Wg + S::OW2 + 4 * t4) : f4{0.f, 0.f, 0.f, 0.f};
+            }
+            for (int i = tid; i < S::NX; i += NT) sm.x[i] = a.x[idx * S::NX + i];
+#pragma unroll
+            for (int q = 0; q < PER; ++q) {
+                const int t4 = tid + NT * q;
+                if (t4 < N4) *(f4 *)(sm.w2 + 4 * t4) = wv[q];
+            }
         } else {
             for (int i = tid; i < S::NX; i += NT) sm.x[i] = a.x[idx * S::NX + i];
         }
@@ -223,7 +245,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             for (int j = 0; j < S::CT2; ++j) {
                 int o = 16 * j + lr;
                 ov[j] = o < S::C2;
-                wrow[j] = W + S::OW2 + (ov[j] ? o : 0) * S::KC2 + kb;
+                wrow[j] = W2 + (ov[j] ? o : 0) * S::KC2 + kb;
             }
             float bw[3][S::CT2][4];
             auto load = [&](float (&b)[S::CT2][4], int blk) {
@@ -627,7 +649,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     float aA[TI], aB[TI];
                     auto load_a = [&](float (&av)[TI], int ks) {
                         const int o = 4 * ks + lg;
-                        const float *w2 = W + S::OW2 + (o < S::C2 ? o : 0) * S::KC2;
+                        const float *w2 = W2 + (o < S::C2 ? o : 0) * S::KC2;
 #pragma unroll
                         for (int t = 0; t < TI; ++t) av[t] = (o < S::C2 && wo[t] >= 0) ? w2[wo[t]] : 0.0f;
                     };
@@ -689,7 +711,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                     for (int t = 0; t < 2; ++t) {
                         int uv = 16 * t + lr;
-                        av[t] = (o < S::C2 && uv < 25) ? W[S::OW2 + o * S::KC2 + c * 25 + uv] : 0.0f;
+                        av[t] = (o < S::C2 && uv < 25) ? W2[o * S::KC2 + c * 25 + uv] : 0.0f;
                     }
 #pragma unroll
                     for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
@@ -878,7 +900,7 @@ int cpcp_blocks_per_cu() {
     return nb;
 }
 
-constexpr int kSmallMinBlocks = 3, kMediumMinBlocks = 2;
+constexpr int kSmallMinBlocks = 3, kMediumMinBlocks = Medium::STAGE2 ? 1 : 2;
 static_assert(sizeof(SmemCpcp<Small>) * kSmallMinBlocks <= 160 * 1024 &&
                   sizeof(SmemCpcp<Medium>) * kMediumMinBlocks <= 160 * 1024,
               "resident workers per CU fit in the LDS");
