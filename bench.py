@@ -11,6 +11,10 @@ Prints one JSON line.  Extra fields:
                 forward, backward-data, weight-gradient and update
                 multiply-adds, x2) over its average launch time, against the
                 MI355X FP32 peak
+  update_stream the training kernel's shared-weight update stream (one fp32
+                atomic add per parameter per sample, performed at the memory
+                side) in adds/s, next to a plain atomic kernel timed on the
+                same footprint (torch's index_add_)
   cpu_baseline  the CPU oracle (sequential per-sample SGD, one core) on a
                 bounded sample of the same workload
   rows          training throughput of the small and medium nets and of
@@ -85,6 +89,31 @@ def measured_traffic(net, workers, samples):
     if t.get("source_sha256") != kernel_source_hash():
         return None
     return t.get("bytes_per_launch")
+
+
+def update_stream(torch, n_params, samples_per_s, sweeps=256):
+    """Atomic adds per second of the Hogwild update stream (every sample adds
+    one fp32 value to each of the n_params shared weights, Section III-A.2),
+    and the rate of torch's index_add_ adding `sweeps` full sweeps of ones
+    into a vector of n_params floats: a plain atomic scatter kernel on the
+    same footprint, timed here."""
+    acc = torch.zeros(n_params, device="cuda")
+    idx = torch.arange(n_params, device="cuda").repeat(sweeps)
+    src = torch.ones(n_params * sweeps, device="cuda")
+    acc.index_add_(0, idx, src)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(3):
+        acc.index_add_(0, idx, src)
+    b.record()
+    torch.cuda.synchronize()
+    ref = 3 * n_params * sweeps / (a.elapsed_time(b) / 1e3)
+    adds = samples_per_s * n_params
+    del acc, idx, src
+    return {"adds_per_s": adds, "reference_adds_per_s": ref,
+            "reference": f"torch index_add_, {sweeps} sweeps over {n_params} floats",
+            "frac_of_reference": adds / ref}
 
 
 def cpu_baseline(layers, p0, x, y, budget_s=15.0):
@@ -353,6 +382,7 @@ def main():
                                       "tflops": fwd_flops * 10000 / (a.elapsed_time(b) / 1e3) / 1e12,
                                       "n_wrong": int(wrong.item())}
 
+    upd = update_stream(torch, net.n_params, value) if mode != chaos.SEQUENTIAL else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(layers, p0, x, y)
     line = {
         "metric": METRIC,
@@ -374,6 +404,7 @@ def main():
                    "train_flop_per_sample": flops},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_FP32_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_FP32_TFLOPS, "traffic": traffic},
+        "update_stream": upd,
         "cpu_baseline": cpu,
         "rows": rows,
         "wall_s": wall,

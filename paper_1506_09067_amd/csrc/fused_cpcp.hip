@@ -96,6 +96,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         sm.koff2[k] = (k < S::KC2) ? c * S::NP1 + u * S::Q1 + v : 0;
     }
 
+    // Training: thread 0 claims the worker's next sample as soon as the
+    // current one is known (Section III-A.1), so the claim's round trip to
+    // the shared counter overlaps a whole sample instead of starting it.
+    int next = -1;
     for (int64_t step = 0;; ++step) {
         // opaque thread index: keeps per-phase index arithmetic inside its phase
         int tid_l = threadIdx.x;
@@ -103,8 +107,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         const int tid = tid_l, lane = tid_l & 63, lr = lane & 15, lg = lane >> 4;
         const int wave = __builtin_amdgcn_readfirstlane(tid_l >> 6);
 
-        if (tid == 0) sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1)
-                                      : (int64_t)blockIdx.x + step * gridDim.x;
+        if (tid == 0) {
+            if (kTrain) sm.idx = (next >= 0) ? next : atomicAdd(a.counter, 1);
+            else sm.idx = (int64_t)blockIdx.x + step * gridDim.x;
+        }
         // Reads are on demand.  Every wavefront first waits for its own
         // pushes of the previous sample to complete (the worker sees its own
         // updates: one worker is exact per-sample SGD); then one wavefront
@@ -116,8 +122,9 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         __syncthreads();
         const int64_t idx = sm.idx;
         if (idx >= a.n) break;
-        if (kTrain) {
-            if (a.claims && tid == 0) atomicAdd(a.claims + idx, 1);
+        if (kTrain && tid == 0) {
+            next = atomicAdd(a.counter, 1);
+            if (a.claims) atomicAdd(a.claims + idx, 1);
         }
         const int label = a.labels[idx];
         if constexpr (S::STAGE) {
