@@ -634,8 +634,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             // address, and wave_lds_order() keeps the overlapping groups in
             // order (plain read-add-write, no atomics).  Seven row tiles per
             // block, computed in passes of four and three.
-            for (int blk = wave; blk < S::C1 / 4; blk += NW) {
-                const int c0 = 4 * blk;
+            auto block4 = [&](const int c0) {
 #pragma unroll
                 for (int pass = 0; pass < 2; ++pass) {
                     constexpr int TI = 4;
@@ -700,6 +699,78 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                             wave_lds_order();
                         }
                 }
+            };
+            // One input map alone: rows uv = 16t + q (two tiles).  The four
+            // lane groups of an accumulator element then hold four (u,v) of
+            // the same map, so each scatter step is done one lane group at a
+            // time (plain read-add-write, groups kept in order).
+            auto map1 = [&](const int c) {
+                f4 acc[2][RT2];
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
+                float aA[2], aB[2];
+                auto load_a = [&](float (&av)[2], int ks) {
+                    const int o = 4 * ks + lg;
+                    const float *w2 = W2 + (o < S::C2 ? o : 0) * S::KC2 + c * 25;
+#pragma unroll
+                    for (int t = 0; t < 2; ++t) {
+                        const int uv = 16 * t + lr;
+                        const float v = w2[uv < 25 ? uv : 0];
+                        av[t] = (o < S::C2 && uv < 25) ? v : 0.0f;
+                    }
+                };
+                auto compute = [&](const float (&av)[2], int ks) {
+                    const int o = 4 * ks + lg;
+                    float bv[RT2];
+#pragma unroll
+                    for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
+#pragma unroll
+                    for (int t = 0; t < 2; ++t)
+#pragma unroll
+                        for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
+                };
+                load_a(aA, 0);
+                for (int ks = 0; ks < S::OKS; ks += 2) {
+                    if (ks + 1 < S::OKS) load_a(aB, ks + 1);
+                    compute(aA, ks);
+                    if (ks + 1 < S::OKS) {
+                        if (ks + 2 < S::OKS) load_a(aA, ks + 2);
+                        compute(aB, ks + 1);
+                    }
+                }
+                float *dp[RT2];
+                bool pvv[RT2];
+#pragma unroll
+                for (int j = 0; j < RT2; ++j) {
+                    const int p = 16 * j + lr;
+                    pvv[j] = p < S::NY2;
+                    const int py = p / S::H2, px = p - py * S::H2;
+                    dp[j] = sm.e1 + c * S::NP1 + (pvv[j] ? py * S::Q1 + px : 0);
+                }
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) {
+                            const int uv = 16 * t + 4 * g + r, u = uv / 5, v = uv - 5 * u;
+                            if (uv >= 25) continue;
+                            if (lg == g) {
+#pragma unroll
+                                for (int j = 0; j < RT2; ++j)
+                                    if (pvv[j]) dp[j][u * S::Q1 + v] += acc[t][j][r];
+                            }
+                            wave_lds_order();
+                        }
+            };
+            if constexpr (S::C1 == 5 * NW) {
+                // five maps per wavefront: a 4-map block and one map alone
+                block4(5 * wave);
+                map1(5 * wave + 4);
+            } else {
+                for (int blk = wave; blk < S::C1 / 4; blk += NW) block4(4 * blk);
             }
         } else {
             // Wavefront w owns input maps c = w, w+4, ... (25 rows each, 2

@@ -176,10 +176,14 @@ def test_hogwild_one_worker_is_sequential(chaos, torch_cuda, name):
             f"{int(torch.nonzero(dl > 0)[0]) if (dl > 0).any() else -1})")
 
 
+@pytest.mark.parametrize("name", ["small", "medium", "large", "large_table1"])
 @pytest.mark.parametrize("mode", ["HOGWILD_ATOMIC", "HOGWILD_RACY"])
-def test_lr_zero_and_claims_once(chaos, torch_cuda, mode):
+def test_lr_zero_and_claims_once(chaos, torch_cuda, mode, name):
+    # every resident worker claims samples (one ahead in the small/medium
+    # kernel); each sample is processed exactly once and, with lr = 0, at the
+    # initial weights
     torch = torch_cuda
-    net, layers, p = _net(chaos, "large")
+    net, layers, p = _net(chaos, name)
     n = 3001
     x, y = wl.train_set(n)
     xd, yd = _dev(torch, x, torch.float32), _dev(torch, y, torch.int32)
