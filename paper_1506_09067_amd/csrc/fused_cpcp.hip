@@ -626,6 +626,71 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 
         // ---- conv2 backward data: C[(c,u,v)][p] = sum_o W2[o][c][u][v] d2[o][p],
         //      col2im into e1[c][p + (u,v)]. ----
+        // One input map alone: rows uv = 16t + q (two tiles).  The four
+        // lane groups of an accumulator element then hold four (u,v) of
+        // the same map, so each scatter step is done one lane group at a
+        // time (plain read-add-write, groups kept in order).
+        auto map1 = [&](const int c) {
+            f4 acc[2][RT2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
+            float aA[2], aB[2];
+            auto load_a = [&](float (&av)[2], int ks) {
+                const int o = 4 * ks + lg;
+                const float *w2 = W2 + (o < S::C2 ? o : 0) * S::KC2 + c * 25;
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+                    const int uv = 16 * t + lr;
+                    const float v = w2[uv < 25 ? uv : 0];
+                    av[t] = (o < S::C2 && uv < 25) ? v : 0.0f;
+                }
+            };
+            auto compute = [&](const float (&av)[2], int ks) {
+                const int o = 4 * ks + lg;
+                float bv[RT2];
+#pragma unroll
+                for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
+            };
+            load_a(aA, 0);
+            for (int ks = 0; ks < S::OKS; ks += 2) {
+                if (ks + 1 < S::OKS) load_a(aB, ks + 1);
+                compute(aA, ks);
+                if (ks + 1 < S::OKS) {
+                    if (ks + 2 < S::OKS) load_a(aA, ks + 2);
+                    compute(aB, ks + 1);
+                }
+            }
+            float *dp[RT2];
+            bool pvv[RT2];
+#pragma unroll
+            for (int j = 0; j < RT2; ++j) {
+                const int p = 16 * j + lr;
+                pvv[j] = p < S::NY2;
+                const int py = p / S::H2, px = p - py * S::H2;
+                dp[j] = sm.e1 + c * S::NP1 + (pvv[j] ? py * S::Q1 + px : 0);
+            }
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const int uv = 16 * t + 4 * g + r, u = uv / 5, v = uv - 5 * u;
+                        if (uv >= 25) continue;
+                        if (lg == g) {
+#pragma unroll
+                            for (int j = 0; j < RT2; ++j)
+                                if (pvv[j]) dp[j][u * S::Q1 + v] += acc[t][j][r];
+                        }
+                        wave_lds_order();
+                    }
+        };
         if constexpr (S::C1 % 4 == 0) {
             // Input maps in blocks of 4, a block owned by one wavefront.  Row
             // q of tile i holds map c0 + q/4 at uv = 4i + q%4, so the four
@@ -700,71 +765,6 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                         }
                 }
             };
-            // One input map alone: rows uv = 16t + q (two tiles).  The four
-            // lane groups of an accumulator element then hold four (u,v) of
-            // the same map, so each scatter step is done one lane group at a
-            // time (plain read-add-write, groups kept in order).
-            auto map1 = [&](const int c) {
-                f4 acc[2][RT2];
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
-                float aA[2], aB[2];
-                auto load_a = [&](float (&av)[2], int ks) {
-                    const int o = 4 * ks + lg;
-                    const float *w2 = W2 + (o < S::C2 ? o : 0) * S::KC2 + c * 25;
-#pragma unroll
-                    for (int t = 0; t < 2; ++t) {
-                        const int uv = 16 * t + lr;
-                        const float v = w2[uv < 25 ? uv : 0];
-                        av[t] = (o < S::C2 && uv < 25) ? v : 0.0f;
-                    }
-                };
-                auto compute = [&](const float (&av)[2], int ks) {
-                    const int o = 4 * ks + lg;
-                    float bv[RT2];
-#pragma unroll
-                    for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
-#pragma unroll
-                    for (int t = 0; t < 2; ++t)
-#pragma unroll
-                        for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
-                };
-                load_a(aA, 0);
-                for (int ks = 0; ks < S::OKS; ks += 2) {
-                    if (ks + 1 < S::OKS) load_a(aB, ks + 1);
-                    compute(aA, ks);
-                    if (ks + 1 < S::OKS) {
-                        if (ks + 2 < S::OKS) load_a(aA, ks + 2);
-                        compute(aB, ks + 1);
-                    }
-                }
-                float *dp[RT2];
-                bool pvv[RT2];
-#pragma unroll
-                for (int j = 0; j < RT2; ++j) {
-                    const int p = 16 * j + lr;
-                    pvv[j] = p < S::NY2;
-                    const int py = p / S::H2, px = p - py * S::H2;
-                    dp[j] = sm.e1 + c * S::NP1 + (pvv[j] ? py * S::Q1 + px : 0);
-                }
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-#pragma unroll
-                        for (int g = 0; g < 4; ++g) {
-                            const int uv = 16 * t + 4 * g + r, u = uv / 5, v = uv - 5 * u;
-                            if (uv >= 25) continue;
-                            if (lg == g) {
-#pragma unroll
-                                for (int j = 0; j < RT2; ++j)
-                                    if (pvv[j]) dp[j][u * S::Q1 + v] += acc[t][j][r];
-                            }
-                            wave_lds_order();
-                        }
-            };
             if constexpr (S::C1 == 5 * NW) {
                 // five maps per wavefront: a 4-map block and one map alone
                 block4(5 * wave);
@@ -773,50 +773,8 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 for (int blk = wave; blk < S::C1 / 4; blk += NW) block4(4 * blk);
             }
         } else {
-            // Wavefront w owns input maps c = w, w+4, ... (25 rows each, 2
-            // tiles), so the LDS atomic adds into a map come from one
-            // wavefront in program order: reproducible.
-            for (int c = wave; c < S::C1; c += NW) {
-                f4 acc[2][RT2];
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
-                for (int ks = 0; ks < S::OKS; ++ks) {
-                    int o = 4 * ks + lg;
-                    float av[2], bv[RT2];
-#pragma unroll
-                    for (int t = 0; t < 2; ++t) {
-                        int uv = 16 * t + lr;
-                        av[t] = (o < S::C2 && uv < 25) ? W2[o * S::KC2 + c * 25 + uv] : 0.0f;
-                    }
-#pragma unroll
-                    for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
-#pragma unroll
-                    for (int t = 0; t < 2; ++t)
-#pragma unroll
-                        for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
-                }
-                float *ec = sm.e1 + c * S::NP1;
-#pragma unroll
-                for (int j = 0; j < RT2; ++j) {
-                    int p = 16 * j + lr;
-                    if (p >= S::NY2) continue;
-                    int py = p / S::H2, px = p - py * S::H2;
-                    float *ep = ec + py * S::Q1 + px;
-#pragma unroll
-                    for (int t = 0; t < 2; ++t)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            int uv = 16 * t + 4 * lg + r;
-                            int u = uv / 5, v = uv - 5 * u;
-                            if (uv < 25)
-                                __hip_atomic_fetch_add(ep + u * S::Q1 + v, acc[t][j][r], __ATOMIC_RELAXED,
-                                                       __HIP_MEMORY_SCOPE_WORKGROUP);
-                        }
-                }
-            }
+            // wavefront w owns input maps w, w + 4, ...
+            for (int c = wave; c < S::C1; c += NW) map1(c);
         }
         __syncthreads();
 

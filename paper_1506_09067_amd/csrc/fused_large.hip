@@ -760,7 +760,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         // maps 5w..5w+4, so col2im needs no ordering between wavefronts.
         // Tiles 0..2 hold maps 5w + q/4 at uv = 4i + q%4 (no two lanes of one
         // scatter instruction on one address, as for conv3); tile 3 holds map
-        // 5w + 4 at uv = q.
+        // 5w + 4 at uv = q and is scattered one lane group at a time.
         {
             f4 acc[4][8];
 #pragma unroll
@@ -806,7 +806,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             }
             // tiles 0..2: scatter grouped by kernel offset uv (distinct
             // addresses inside a group, groups kept in order); tile 3 (one
-            // map, lanes at different uv may meet): LDS atomics
+            // map, lanes at different uv may meet): one lane group per step
             float *e1 = sm.s2;
             float *dp[8];
             bool pv[8];
@@ -828,18 +828,21 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                         if (pv[j]) dp[j][(c0 + lg) * NP1 + u * Q1 + v] += acc[i][j][r];
                     wave_lds_order();
                 }
+            // tile 3: the four lane groups hold four (u,v) of the same map, so
+            // each scatter step is done one lane group at a time (in order)
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                if (!pv[j]) continue;
-                float *d4 = dp[j] + (c0 + 4) * NP1;
+            for (int g = 0; g < 3; ++g)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    int uv = 4 * lg + r, u = uv / 3, v = uv - 3 * u;
-                    if (uv < 9)
-                        __hip_atomic_fetch_add(d4 + u * Q1 + v, acc[3][j][r], __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_WORKGROUP);
+                    const int uv = 4 * g + r, u = uv / 3, v = uv - 3 * u;
+                    if (uv >= 9) continue;
+                    if (lg == g) {
+#pragma unroll
+                        for (int j = 0; j < 8; ++j)
+                            if (pv[j]) dp[j][(c0 + 4) * NP1 + u * Q1 + v] += acc[3][j][r];
+                    }
+                    wave_lds_order();
                 }
-            }
         }
         __syncthreads();
 
