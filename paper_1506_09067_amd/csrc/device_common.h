@@ -102,6 +102,22 @@ __device__ __forceinline__ void wait_vector_memory() {
     __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
+// One ordered step of a col2im scatter in LDS: this lane adds c[j] to
+// p[j][off] for every j.  The J reads are issued together, then the J
+// writes, with no branch between them: a lane whose column is padding points
+// its p[j] at a scratch area instead (of at least off + 1 floats), so the
+// targets of one step are distinct across j and across the lanes of an
+// instruction.  Steps whose targets overlap stay in program order.
+template <int J>
+__device__ __forceinline__ void scatter_add(float *const (&p)[J], int off, const float (&c)[J]) {
+    float old[J];
+#pragma unroll
+    for (int j = 0; j < J; ++j) old[j] = p[j][off];
+#pragma unroll
+    for (int j = 0; j < J; ++j) p[j][off] = old[j] + c[j];
+    wave_lds_order();
+}
+
 // Workgroup barrier that orders LDS only: the wavefronts' outstanding global
 // memory operations (weight pushes) stay in flight across it.
 __device__ __forceinline__ void lds_barrier() {

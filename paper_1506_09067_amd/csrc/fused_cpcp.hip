@@ -75,6 +75,7 @@ struct alignas(16) SmemCpcp {
     unsigned char am2[S::NF1 + 16];
     alignas(16) float w[S::STAGE ? S::NPARAM4 : 4];  // the weights read at the start of the sample
     alignas(16) float w2[S::STAGE2 ? S::NW2 : 4];    // the conv2 weights read at the start of the sample
+    float sink[64];                      // scatter target of padding lanes
     int64_t idx;
 };
 
@@ -667,14 +668,13 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 }
             }
             float *dp[RT2];
-            bool pvv[RT2];
 #pragma unroll
             for (int j = 0; j < RT2; ++j) {
                 const int p = 16 * j + lr;
-                pvv[j] = p < S::NY2;
                 const int py = p / S::H2, px = p - py * S::H2;
-                dp[j] = sm.e1 + c * S::NP1 + (pvv[j] ? py * S::Q1 + px : 0);
+                dp[j] = (p < S::NY2) ? sm.e1 + c * S::NP1 + py * S::Q1 + px : sm.sink;
             }
+            // each step serves one lane group
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -684,11 +684,13 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                         const int uv = 16 * t + 4 * g + r, u = uv / 5, v = uv - 5 * u;
                         if (uv >= 25) continue;
                         if (lg == g) {
+                            float cv[RT2];
 #pragma unroll
-                            for (int j = 0; j < RT2; ++j)
-                                if (pvv[j]) dp[j][u * S::Q1 + v] += acc[t][j][r];
+                            for (int j = 0; j < RT2; ++j) cv[j] = acc[t][j][r];
+                            scatter_add<RT2>(dp, u * S::Q1 + v, cv);
+                        } else {
+                            wave_lds_order();
                         }
-                        wave_lds_order();
                     }
         };
         if constexpr (S::C1 % 4 == 0) {
@@ -744,13 +746,11 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                         }
                     }
                     float *dp[RT2];
-                    bool pvv[RT2];
 #pragma unroll
                     for (int j = 0; j < RT2; ++j) {
                         const int p = 16 * j + lr;
-                        pvv[j] = p < S::NY2;
                         const int py = p / S::H2, px = p - py * S::H2;
-                        dp[j] = sm.e1 + (c0 + lg) * S::NP1 + (pvv[j] ? py * S::Q1 + px : 0);
+                        dp[j] = (p < S::NY2) ? sm.e1 + (c0 + lg) * S::NP1 + py * S::Q1 + px : sm.sink;
                     }
 #pragma unroll
                     for (int t = 0; t < TI; ++t)
@@ -758,10 +758,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                         for (int r = 0; r < 4; ++r) {
                             const int uv = 4 * (i0 + t) + r, u = uv / 5, v = uv - 5 * u;
                             if (t >= nt || uv >= 25) continue;
+                            float c[RT2];
 #pragma unroll
-                            for (int j = 0; j < RT2; ++j)
-                                if (pvv[j]) dp[j][u * S::Q1 + v] += acc[t][j][r];
-                            wave_lds_order();
+                            for (int j = 0; j < RT2; ++j) c[j] = acc[t][j][r];
+                            scatter_add<RT2>(dp, u * S::Q1 + v, c);
                         }
                 }
             };

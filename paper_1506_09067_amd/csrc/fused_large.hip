@@ -78,6 +78,7 @@ struct alignas(16) Smem {
     alignas(16) int koff2[KC2 + 4];      // im2col offset into p1 of k = (c,u,v), conv2
     unsigned char am1[C1 * NP1 + 12];    // pool1 argmax (window element 0..3)
     unsigned char am3[NF1 + 4];          // pool2 argmax
+    float sink[128];                     // scatter target of padding lanes
     int64_t idx;
 };
 static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
@@ -652,25 +653,21 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             }
             float *dst = sm.s2 + (4 * blk + lg) * NY2;
             float *dm[3];
-            bool mv[3];
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
                 int m = 16 * j + lr;
-                mv[j] = m < M3;
-                dm[j] = dst + (mv[j] ? window_pos(m >> 2, m & 3, 3, H2) : 0);
+                dm[j] = (m < M3) ? dst + window_pos(m >> 2, m & 3, 3, H2) : sm.sink;
             }
             // scatter grouped by kernel offset uv: inside a group the 3 x 64
-            // lanes write distinct addresses; wave_lds_order() orders the
-            // groups, whose targets overlap
+            // lanes write distinct addresses; the groups, whose targets
+            // overlap, stay in order
 #pragma unroll
             for (int i = 0; i < 9; ++i)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int uv = 4 * i + r, u = uv / 6, v = uv - 6 * u;
-#pragma unroll
-                    for (int j = 0; j < 3; ++j)
-                        if (mv[j]) dm[j][u * H2 + v] += acc[i][j][r];
-                    wave_lds_order();
+                    const float c[3] = {acc[i][0][r], acc[i][1][r], acc[i][2][r]};
+                    scatter_add<3>(dm, u * H2 + v, c);
                 }
         }
         __syncthreads();
@@ -808,14 +805,13 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             // addresses inside a group, groups kept in order); tile 3 (one
             // map, lanes at different uv may meet): one lane group per step
             float *e1 = sm.s2;
-            float *dp[8];
-            bool pv[8];
+            float *dp[8], *dq[8];  // this lane's column in map c0 + lg and in map c0 + 4
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
                 int p = 16 * j + lr;
-                pv[j] = p < NY2;
                 int py = p / H2, px = p - py * H2;
-                dp[j] = e1 + (pv[j] ? py * Q1 + px : 0);
+                dp[j] = (p < NY2) ? e1 + (c0 + lg) * NP1 + py * Q1 + px : sm.sink;
+                dq[j] = (p < NY2) ? e1 + (c0 + 4) * NP1 + py * Q1 + px : sm.sink;
             }
 #pragma unroll
             for (int i = 0; i < 3; ++i)
@@ -823,13 +819,13 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 for (int r = 0; r < 4; ++r) {
                     const int uv = 4 * i + r, u = uv / 3, v = uv - 3 * u;
                     if (uv >= 9) continue;
+                    float c[8];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        if (pv[j]) dp[j][(c0 + lg) * NP1 + u * Q1 + v] += acc[i][j][r];
-                    wave_lds_order();
+                    for (int j = 0; j < 8; ++j) c[j] = acc[i][j][r];
+                    scatter_add<8>(dp, u * Q1 + v, c);
                 }
             // tile 3: the four lane groups hold four (u,v) of the same map, so
-            // each scatter step is done one lane group at a time (in order)
+            // each scatter step serves one lane group
 #pragma unroll
             for (int g = 0; g < 3; ++g)
 #pragma unroll
@@ -837,11 +833,13 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     const int uv = 4 * g + r, u = uv / 3, v = uv - 3 * u;
                     if (uv >= 9) continue;
                     if (lg == g) {
+                        float c[8];
 #pragma unroll
-                        for (int j = 0; j < 8; ++j)
-                            if (pv[j]) dp[j][(c0 + 4) * NP1 + u * Q1 + v] += acc[3][j][r];
+                        for (int j = 0; j < 8; ++j) c[j] = acc[3][j][r];
+                        scatter_add<8>(dq, u * Q1 + v, c);
+                    } else {
+                        wave_lds_order();
                     }
-                    wave_lds_order();
                 }
         }
         __syncthreads();

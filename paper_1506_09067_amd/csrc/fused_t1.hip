@@ -82,6 +82,7 @@ struct alignas(16) Smem {
     alignas(16) int koff3[KC3];          // im2col offset into y2 of k = (c,u,v), conv3
     alignas(16) int koff2[KC2P];         // im2col offset into a1 of k = (c,u,v), conv2 (0 past KC2)
     unsigned char am3[NF1 + 4];          // pool2 argmax
+    float sink[128];                     // scatter target of padding lanes
     int64_t idx;
 };
 static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
@@ -658,25 +659,21 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
             }
             float *dst = sm.s2 + (4 * blk + lg) * NY2;
             float *dm[3];
-            bool mv[3];
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
                 int m = 16 * j + lr;
-                mv[j] = m < M3;
-                dm[j] = dst + (mv[j] ? window_pos(m >> 2, m & 3, 3, H2) : 0);
+                dm[j] = (m < M3) ? dst + window_pos(m >> 2, m & 3, 3, H2) : sm.sink;
             }
             // scatter grouped by kernel offset uv: inside a group the 3 x 64
-            // lanes write distinct addresses; wave_lds_order() orders the
-            // groups, whose targets overlap
+            // lanes write distinct addresses; the groups, whose targets
+            // overlap, stay in order
 #pragma unroll
             for (int i = 0; i < 9; ++i)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int uv = 4 * i + r, u = uv / 6, v = uv - 6 * u;
-#pragma unroll
-                    for (int j = 0; j < 3; ++j)
-                        if (mv[j]) dm[j][u * H2 + v] += acc[i][j][r];
-                    wave_lds_order();
+                    const float c[3] = {acc[i][0][r], acc[i][1][r], acc[i][2][r]};
+                    scatter_add<3>(dm, u * H2 + v, c);
                 }
         }
         __syncthreads();
@@ -829,13 +826,12 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 // scatter: element r of tile i is (u,v) = uv 4i + r of map
                 // c0 + lg; column m = 4P + w is conv2 output (2py + w/2, 2px + w%2)
                 float *dp[4];
-                bool mv[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int m = 16 * (j0 + j) + lr, P = m >> 2, w = m & 3;
                     const int py = P / Q2, px = P - py * Q2;
-                    mv[j] = m < M2;
-                    dp[j] = sm.e1 + (c0 + lg) * NA1 + (mv[j] ? (2 * py + (w >> 1)) * H1 + 2 * px + (w & 1) : 0);
+                    dp[j] = (m < M2) ? sm.e1 + (c0 + lg) * NA1 + (2 * py + (w >> 1)) * H1 + 2 * px + (w & 1)
+                                     : sm.sink;
                 }
 #pragma unroll
                 for (int i = 0; i < 7; ++i)
@@ -843,10 +839,8 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     for (int r = 0; r < 4; ++r) {
                         const int uv = 4 * i + r, u = uv / 5, v = uv - 5 * u;
                         if (uv >= 25) continue;
-#pragma unroll
-                        for (int j = 0; j < 4; ++j)
-                            if (mv[j]) dp[j][u * H1 + v] += acc[i][j][r];
-                        wave_lds_order();
+                        const float c[4] = {acc[i][0][r], acc[i][1][r], acc[i][2][r], acc[i][3][r]};
+                        scatter_add<4>(dp, u * H1 + v, c);
                     }
             }
         };
