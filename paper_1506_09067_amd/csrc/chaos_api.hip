@@ -25,7 +25,7 @@ struct chaos_net {
     int cpcp = 0;                 // fused small (1) / medium (2) kernel serves this net
     int max_workers = 0;          // resident workers of the training kernel
     float *scratch = nullptr;     // [max_workers][scratch_floats]
-    int32_t *counter = nullptr;   // sample claim counter
+    int32_t *counter = nullptr;   // [0] samples claimed, [1] samples completed (training)
     int fb_workers = 0;           // rows of grad_part
     float *grad_part = nullptr;   // [fb_workers][n_params]
     int32_t *claims = nullptr;    // debug claim counter (caller-owned)
@@ -338,7 +338,7 @@ int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_
         a.claims = net->claims;
         int kmode = mode == CHAOS_HOGWILD_RACY ? chaos::kTrainRacy : chaos::kTrainAtomic;
         int grid = (int)std::min<int64_t>(workers, n);
-        HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 1, stream), "counter reset");
+        HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 2, stream), "counter reset");
         HIP_TRY(chaos::launch_worker(kmode, net->desc, a, grid, 64, stream), "train launch");
         return ok();
     }
@@ -353,7 +353,7 @@ int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_
     a.lr = lr;
     a.loss = loss_dev;
     a.claims = net->claims;
-    HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 1, stream), "counter reset");
+    HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 2, stream), "counter reset");
     HIP_TRY(launch(net, kmode, a, grid, stream), "train launch");
     return ok();
 }

@@ -43,7 +43,7 @@ struct WorkArgs {
     const int32_t *labels;
     int64_t n;
     float lr;
-    int32_t *counter;      // dynamic sample claim (training)
+    int32_t *counter;      // training: [0] samples claimed, [1] samples completed
     float *scratch;        // [workers][scratch_floats]
     float *loss;           // [n] optional
     float *out;            // [n][n_out] optional

@@ -118,6 +118,25 @@ __device__ __forceinline__ void scatter_add(float *const (&p)[J], int off, const
     wave_lds_order();
 }
 
+// Start of a Hogwild epoch.  Every worker of a fused kernel is resident from
+// the launch, so without care all of them would compute their first gradient
+// at the same weights and push it at nearly the same time: a burst of
+// concurrent, identically stale updates.  Instead worker b (b > 0) claims its
+// first sample once b / kJoinRamp samples have been completed (counter[1]) or
+// once every sample has been handed out (counter[0] >= n), so the number of
+// workers grows with the completed samples.  Worker 0 never waits, so the
+// condition is always reached; the poll count is bounded as well.
+constexpr int kJoinRamp = 4;
+
+__device__ __forceinline__ void join_after(int32_t *counter, int64_t n, int target) {
+    for (int s = 0; s < (1 << 20); ++s) {
+        const int done = __hip_atomic_load(counter + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int claimed = __hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (done >= target || claimed >= n) return;
+        __builtin_amdgcn_s_sleep(32);
+    }
+}
+
 // Workgroup barrier that orders LDS only: the wavefronts' outstanding global
 // memory operations (weight pushes) stay in flight across it.
 __device__ __forceinline__ void lds_barrier() {

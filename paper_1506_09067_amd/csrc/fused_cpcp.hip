@@ -109,6 +109,8 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         const int wave = __builtin_amdgcn_readfirstlane(tid_l >> 6);
 
         if (tid == 0) {
+            if (kTrain && next < 0 && blockIdx.x > 0)
+                join_after(a.counter, a.n, (int)blockIdx.x / kJoinRamp);
             if (kTrain) sm.idx = (next >= 0) ? next : atomicAdd(a.counter, 1);
             else sm.idx = (int64_t)blockIdx.x + step * gridDim.x;
         }
@@ -903,6 +905,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 }
             }
         }
+        if (kTrain && tid == 0) atomicAdd(a.counter + 1, 1);  // samples completed
         __syncthreads();
     }
 }

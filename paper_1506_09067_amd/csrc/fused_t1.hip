@@ -110,8 +110,11 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         const int tid = tid_l, lane = tid_l & 63, lr = lane & 15, lg = lane >> 4;
         const int wave = __builtin_amdgcn_readfirstlane(tid_l >> 6);
         // ---- claim a sample (Section III-A.1) ----
-        if (tid == 0) sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1)
-                                      : (int64_t)blockIdx.x + step * gridDim.x;
+        if (tid == 0) {
+            if (kTrain && step == 0 && blockIdx.x > 0)
+                join_after(a.counter, a.n, (int)blockIdx.x / kJoinRamp);
+            sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1) : (int64_t)blockIdx.x + step * gridDim.x;
+        }
         // Reads are on demand.  Every wavefront first waits for its own
         // pushes of the previous sample to complete (the worker sees its own
         // updates: one worker is exact per-sample SGD); then one wavefront
@@ -976,6 +979,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 }
             }
         }
+        if (kTrain && tid == 0) atomicAdd(a.counter + 1, 1);  // samples completed
         __syncthreads();
     }
 }
