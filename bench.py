@@ -264,6 +264,41 @@ def model_fit(chaos, wl, torch, name):
     }
 
 
+def training_session(chaos, wl, torch, name, epochs, lr, decay, seq_epochs):
+    """A whole training session (Section III-A.1): per epoch Training over the
+    60,000-sample set, Validation on it and Testing on the 10,000-sample set,
+    with every resident worker (Hogwild, atomic pushes), timed as one call;
+    then the same session with one worker (sequential per-sample SGD) for
+    `seq_epochs` epochs, for the per-epoch comparison and the speed-up."""
+    layers = wl.NETS[name]
+    p0 = wl.init_params(layers)
+    x, y = wl.train_set(60000)
+    xt, yt = wl.test_set(10000)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    xtd, ytd = torch.from_numpy(xt).cuda(), torch.from_numpy(yt).cuda()
+
+    def run(mode, n_epochs):
+        net = chaos.Net(layers, p0)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        st = net.train_session(xd, yd, xtd, ytd, n_epochs, lr, decay, mode=mode)
+        b.record()
+        torch.cuda.synchronize()
+        rows = [{"epoch": e + 1, "train_loss": float(r[0]), "train_wrong": int(r[1]),
+                 "test_wrong": int(r[2]), "test_loss": float(r[3])}
+                for e, r in enumerate(st.cpu().tolist())]
+        return rows, a.elapsed_time(b) / 1e3, net.max_workers
+
+    hog, t_hog, workers = run(chaos.HOGWILD_ATOMIC, epochs)
+    seq, t_seq, _ = run(chaos.SEQUENTIAL, seq_epochs) if seq_epochs else ([], None, 1)
+    out = {"session": f"{name} net, 60000 training + 10000 test samples, lr {lr} x {decay}/epoch",
+           "hogwild": {"workers": workers, "epochs": epochs, "seconds": t_hog, "per_epoch": hog}}
+    if seq_epochs:
+        out["sequential"] = {"workers": 1, "epochs": seq_epochs, "seconds": t_seq, "per_epoch": seq}
+        out["speedup_per_epoch"] = (t_seq / seq_epochs) / (t_hog / epochs)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -283,6 +318,13 @@ def main():
                     help="instead of the benchmark line, fit the Section III-C performance "
                          "model to measurements of --net and print its parameters, its "
                          "prediction accuracy and a what-if table as one JSON line")
+    ap.add_argument("--session", type=int, default=0, metavar="EPOCHS",
+                    help="instead of the benchmark line, run a whole Training + Validation + "
+                         "Testing session of EPOCHS epochs of --net with every resident worker "
+                         "(and --seq-epochs epochs with one worker) and print per-epoch "
+                         "statistics as one JSON line")
+    ap.add_argument("--seq-epochs", type=int, default=1)
+    ap.add_argument("--decay", type=float, default=1.0)
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (calibrates "
                          "the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -311,6 +353,10 @@ def main():
         return
     if args.model:
         print(json.dumps(model_fit(chaos, wl, torch, args.net)), flush=True)
+        return
+    if args.session:
+        print(json.dumps(training_session(chaos, wl, torch, args.net, args.session, 1e-3,
+                                          args.decay, args.seq_epochs)), flush=True)
         return
     layers = wl.NETS[args.net]
     p0 = wl.init_params(layers)
