@@ -117,13 +117,13 @@ int chaos_apply_update(chaos_net *net, const float *grad_dev, float lr, hipStrea
  * Hogwild, III-A.2) with no synchronisation between workers (Arbitrary Order
  * of Synchronization, III-A.3).  workers: number of concurrent workers for
  * the Hogwild modes (0 = chaos_max_workers(net)); ignored by
- * CHAOS_SEQUENTIAL.  The workers of an epoch join as its first samples
- * complete (worker b claims its first sample after b/4 samples have been
- * completed), so that their first gradients are not all taken at the same
- * weights.  Up to chaos_max_workers() the net's own kernel runs;
- * above it, up to chaos_worker_limit(), every worker is one 64-thread
- * wavefront of the generic kernel (per-worker state in HBM, allocated on
- * first use).  Larger values are CHAOS_EINVAL.
+ * CHAOS_SEQUENTIAL.  Up to chaos_max_workers() the net's own kernel runs,
+ * and the workers of an epoch join as its first samples complete (worker b
+ * claims its first sample after b/4 samples have been completed), so that
+ * their first gradients are not all taken at the same weights; above it, up
+ * to chaos_worker_limit(), every worker is one 64-thread wavefront of the
+ * generic kernel (per-worker state in HBM, allocated on first use), all
+ * starting at once.  Larger values are CHAOS_EINVAL.
  * loss_dev [n] (optional): each sample's loss at the time it was processed. */
 int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_dev, int64_t n,
                       float lr, int32_t mode, int32_t workers, float *loss_dev,
