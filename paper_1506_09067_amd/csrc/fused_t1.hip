@@ -288,9 +288,10 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
             auto load_b = [&](f4 (&b)[7], int S) {
 #pragma unroll
                 for (int j = 0; j < 7; ++j) {
+                    // padding columns (o >= C3) read the last map: their
+                    // accumulators are never used, and no branch splits the loads
                     int o = 16 * j + lr;
-                    b[j] = (o < C3) ? *(const f4 *)(W + OW3 + o * KC3 + 16 * S + 4 * lg)
-                                    : f4{0.f, 0.f, 0.f, 0.f};
+                    b[j] = *(const f4 *)(W + OW3 + (o < C3 ? o : C3 - 1) * KC3 + 16 * S + 4 * lg);
                 }
             };
             auto compute = [&](const f4 (&b)[7], int S) {
@@ -300,7 +301,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 for (int s = 0; s < 4; ++s) {
                     float av[3];
 #pragma unroll
-                    for (int i = 0; i < 3; ++i) av[i] = valid[i] ? sm.y2[base[i] + offs[s]] : 0.0f;
+                    for (int i = 0; i < 3; ++i) av[i] = sm.y2[base[i] + offs[s]];  // padding rows: unused
 #pragma unroll
                     for (int i = 0; i < 3; ++i)
 #pragma unroll
