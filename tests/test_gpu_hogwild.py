@@ -47,7 +47,7 @@ def _train_and_test(torch, chaos, name, x, y, xt, yt, epochs, lr, decay, mode, w
 # their first gradients are not all computed at the same weights.
 CASES = [
     ("small", 60000, 5, 1e-3, 0),
-    ("medium", 60000, 1, 1e-3, 0),
+    ("medium", 60000, 3, 1e-3, 0),
     ("large", 60000, 1, 1e-3, 0),
     ("large", 60000, 1, 1e-3, 64),
     ("large_table1", 20000, 1, 1e-3, 0),
