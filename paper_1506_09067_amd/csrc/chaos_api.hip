@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <vector>
 
 using chaos::Layer;
 using chaos::Net;
@@ -18,7 +19,10 @@ struct chaos_net {
     int device = 0;
     Net desc{};
     int64_t n_params = 0;
-    float *params = nullptr;      // shared weights, canonical layout
+    float *params = nullptr;      // shared weights, in the layout of the net's kernel
+    chaos::ParamLayout layout{};  // canonical <-> device layout of params
+    bool padded = false;          // layout is not the identity
+    float *canon = nullptr;       // canonical copy for the generic kernel (padded nets)
     int block = 256;              // threads per worker
     bool fused = false;           // the fused large-net kernel serves this net
     bool t1 = false;              // the fused kernel of Table I's large net serves this net
@@ -227,11 +231,32 @@ int chaos_create_net(int32_t in_h, int32_t in_w, const chaos_layer *layers, int3
     size_t scratch_bytes = (net->fused || net->t1 || net->cpcp)
                                ? 0
                                : (size_t)net->max_workers * desc.scratch_floats * sizeof(float);
-    e = hipMalloc(&net->params, (size_t)n_params * sizeof(float));
+    if (net->fused) {
+        chaos::fused_large_layout(net->layout);
+        net->padded = true;
+    } else {
+        net->layout.n_seg = 1;
+        net->layout.n_dev = (int)n_params;
+        net->layout.seg[0] = chaos::ParamSegment{0, 0, 1, (int)n_params, (int)n_params};
+    }
+    // the initial weights in the device layout (padding zero)
+    std::vector<float> dev;
+    const float *init = init_params_host;
+    if (net->padded) {
+        dev.assign((size_t)net->layout.n_dev, 0.0f);
+        for (int k = 0; k < net->layout.n_seg; ++k) {
+            const chaos::ParamSegment &g = net->layout.seg[k];
+            for (int r = 0; r < g.rows; ++r)
+                std::memcpy(&dev[(size_t)g.dev_off + (size_t)r * g.dev_stride],
+                            init_params_host + g.can_off + (size_t)r * g.len, (size_t)g.len * sizeof(float));
+        }
+        init = dev.data();
+    }
+    e = hipMalloc(&net->params, (size_t)net->layout.n_dev * sizeof(float));
     if (e == hipSuccess && scratch_bytes) e = hipMalloc(&net->scratch, scratch_bytes);
     if (e == hipSuccess) e = hipMalloc(&net->counter, 64);
     if (e == hipSuccess)
-        e = hipMemcpy(net->params, init_params_host, (size_t)n_params * sizeof(float),
+        e = hipMemcpy(net->params, init, (size_t)net->layout.n_dev * sizeof(float),
                       hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         chaos_destroy_net(net);
@@ -246,6 +271,7 @@ int chaos_destroy_net(chaos_net *net) {
     if (!net) return ok();
     (void)hipSetDevice(net->device);
     (void)hipFree(net->params);
+    (void)hipFree(net->canon);
     (void)hipFree(net->scratch);
     (void)hipFree(net->counter);
     (void)hipFree(net->grad_part);
@@ -280,9 +306,14 @@ int chaos_get_params(const chaos_net *net, float *dst_dev, hipStream_t stream) {
     if (int rc = check_net(net)) return rc;
     if (!dst_dev) return fail(CHAOS_EINVAL, "dst_dev is NULL");
     if (int rc = set_device(net)) return rc;
-    HIP_TRY(hipMemcpyAsync(dst_dev, net->params, (size_t)net->n_params * sizeof(float),
-                           hipMemcpyDeviceToDevice, stream),
-            "get_params");
+    if (net->padded)
+        HIP_TRY(chaos::launch_convert_params(net->params, dst_dev, net->layout, net->n_params, false,
+                                             stream),
+                "get_params");
+    else
+        HIP_TRY(hipMemcpyAsync(dst_dev, net->params, (size_t)net->n_params * sizeof(float),
+                               hipMemcpyDeviceToDevice, stream),
+                "get_params");
     return ok();
 }
 
@@ -290,9 +321,14 @@ int chaos_set_params(chaos_net *net, const float *src_dev, hipStream_t stream) {
     if (int rc = check_net(net)) return rc;
     if (!src_dev) return fail(CHAOS_EINVAL, "src_dev is NULL");
     if (int rc = set_device(net)) return rc;
-    HIP_TRY(hipMemcpyAsync(net->params, src_dev, (size_t)net->n_params * sizeof(float),
-                           hipMemcpyDeviceToDevice, stream),
-            "set_params");
+    if (net->padded)
+        HIP_TRY(chaos::launch_convert_params(src_dev, net->params, net->layout, net->n_params, true,
+                                             stream),
+                "set_params");
+    else
+        HIP_TRY(hipMemcpyAsync(net->params, src_dev, (size_t)net->n_params * sizeof(float),
+                               hipMemcpyDeviceToDevice, stream),
+                "set_params");
     return ok();
 }
 
@@ -306,7 +342,11 @@ int chaos_apply_update(chaos_net *net, const float *grad_dev, float lr, hipStrea
     if (int rc = check_net(net)) return rc;
     if (!grad_dev) return fail(CHAOS_EINVAL, "grad_dev is NULL");
     if (int rc = set_device(net)) return rc;
-    HIP_TRY(chaos::launch_axpy(net->params, grad_dev, -lr, net->n_params, stream), "apply_update");
+    if (net->padded)
+        HIP_TRY(chaos::launch_axpy_mapped(net->params, grad_dev, -lr, net->layout, net->n_params, stream),
+                "apply_update");
+    else
+        HIP_TRY(chaos::launch_axpy(net->params, grad_dev, -lr, net->n_params, stream), "apply_update");
     return ok();
 }
 
@@ -331,15 +371,33 @@ int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_
                 return fail(CHAOS_ENOMEM, "scratch for %d workers", net->worker_limit);
             }
         }
+        // the generic kernel reads the canonical layout: a padded net's
+        // weights are copied to it and back around the launch
+        if (net->padded && !net->canon) {
+            if (hipMalloc(&net->canon, (size_t)net->n_params * sizeof(float)) != hipSuccess) {
+                net->canon = nullptr;
+                return fail(CHAOS_ENOMEM, "canonical weights for the generic kernel");
+            }
+        }
         chaos::WorkArgs a = base_args(net, x_dev, labels_dev, n);
         a.scratch = net->wide_scratch;
         a.lr = lr;
         a.loss = loss_dev;
         a.claims = net->claims;
+        if (net->padded) {
+            a.params = net->canon;
+            HIP_TRY(chaos::launch_convert_params(net->params, net->canon, net->layout, net->n_params,
+                                                 false, stream),
+                    "to canonical");
+        }
         int kmode = mode == CHAOS_HOGWILD_RACY ? chaos::kTrainRacy : chaos::kTrainAtomic;
         int grid = (int)std::min<int64_t>(workers, n);
         HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 2, stream), "counter reset");
         HIP_TRY(chaos::launch_worker(kmode, net->desc, a, grid, 64, stream), "train launch");
+        if (net->padded)
+            HIP_TRY(chaos::launch_convert_params(net->canon, net->params, net->layout, net->n_params,
+                                                 true, stream),
+                    "to device layout");
         return ok();
     }
     int grid = 1;

@@ -53,6 +53,21 @@ struct WorkArgs {
     int32_t *claims;       // [n] optional debug claim counter
 };
 
+// Device layout of a net's shared weights, as segments of the canonical
+// vector: segment s holds rows r < rows of len floats, at can_off + r * len
+// in the canonical layout and at dev_off + r * dev_stride on the device.
+// The identity layout is one segment.  Device floats outside every segment
+// are padding.
+struct ParamSegment {
+    int can_off, dev_off, rows, len, dev_stride;
+};
+constexpr int kMaxSegments = 12;
+struct ParamLayout {
+    int n_seg;
+    int n_dev;  // device floats
+    ParamSegment seg[kMaxSegments];
+};
+
 // Launchers (worker.hip).  Each returns the hipError_t of the launch.
 hipError_t launch_worker(int mode, const Net &net, const WorkArgs &a, int grid, int block,
                          hipStream_t s);
@@ -61,6 +76,11 @@ hipError_t launch_fill_f32(float *p, float v, int64_t n, hipStream_t s);
 hipError_t launch_reduce_partials(const float *part, int64_t rows, int64_t cols, float *dst,
                                   hipStream_t s);
 hipError_t launch_axpy(float *w, const float *g, float alpha, int64_t n, hipStream_t s);
+// canonical <-> device copies, and w_dev += alpha * g_canonical, under a layout
+hipError_t launch_convert_params(const float *src, float *dst, const ParamLayout &L, int64_t n_can,
+                                 bool to_device, hipStream_t s);
+hipError_t launch_axpy_mapped(float *w_dev, const float *g_can, float alpha, const ParamLayout &L,
+                              int64_t n_can, hipStream_t s);
 hipError_t launch_mean(const float *v, int64_t n, float *dst, hipStream_t s);
 hipError_t launch_count(const int32_t *src, float *dst, hipStream_t s);
 // Occupancy of the worker kernel: resident blocks per CU for a given block size.
@@ -69,6 +89,7 @@ int worker_blocks_per_cu(int block);
 // Fused MFMA worker for the large net (conv20k4, max2, conv60k3, conv100k6,
 // max2, FC150, FC10 on 29x29 inputs); 256 threads per worker, no scratch.
 bool fused_large_matches(const Net &net);
+void fused_large_layout(ParamLayout &L);  // its padded device layout
 hipError_t launch_fused_large(int mode, const WorkArgs &a, int grid, hipStream_t s);
 int fused_large_blocks_per_cu();
 

@@ -42,44 +42,49 @@ struct Push {
     float *each;  // this sample's gradient row or null
     float *part;  // this worker's partial-sum row or null
 
-    __device__ __forceinline__ void operator()(int off, float g) const {
+    // w_off indexes the shared weights (the kernel's device layout), g_off
+    // the gradient rows (canonical layout); they differ only for a net whose
+    // device layout pads its rows.
+    __device__ __forceinline__ void operator()(int w_off, int g_off, float g) const {
         if (mode == kTrainAtomic) {
-            __hip_atomic_fetch_add(params + off, __fmul_rn(neg_lr, g), __ATOMIC_RELAXED,
+            __hip_atomic_fetch_add(params + w_off, __fmul_rn(neg_lr, g), __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
         } else if (mode == kTrainRacy) {
             // same two roundings as the atomic path: w + round(-lr * g)
             // (the library is built without multiply-add contraction)
-            float w = __hip_atomic_load(params + off, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(params + off, __fadd_rn(w, __fmul_rn(neg_lr, g)),
+            float w = __hip_atomic_load(params + w_off, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(params + w_off, __fadd_rn(w, __fmul_rn(neg_lr, g)),
                                __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         } else {
-            if (each) each[off] = g;
+            if (each) each[g_off] = g;
             if (part)
-                __hip_atomic_fetch_add(part + off, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_add(part + g_off, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
+    __device__ __forceinline__ void operator()(int off, float g) const { (*this)(off, off, g); }
 
     // The same push, returning the weight it found: the value just before
     // this push (training) or the unchanged weight (frozen).  A layer whose
     // partial derivatives need its own weights can take them from here in
     // one pass instead of reading them before pushing.
-    __device__ __forceinline__ float with_old(int off, float g) const {
+    __device__ __forceinline__ float with_old(int w_off, int g_off, float g) const {
         if (mode == kTrainAtomic) {
-            return __hip_atomic_fetch_add(params + off, __fmul_rn(neg_lr, g), __ATOMIC_RELAXED,
+            return __hip_atomic_fetch_add(params + w_off, __fmul_rn(neg_lr, g), __ATOMIC_RELAXED,
                                           __HIP_MEMORY_SCOPE_AGENT);
         } else if (mode == kTrainRacy) {
-            float w = __hip_atomic_load(params + off, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(params + off, __fadd_rn(w, __fmul_rn(neg_lr, g)), __ATOMIC_RELAXED,
+            float w = __hip_atomic_load(params + w_off, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(params + w_off, __fadd_rn(w, __fmul_rn(neg_lr, g)), __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
             return w;
         } else {
-            const float w = params[off];
-            if (each) each[off] = g;
+            const float w = params[w_off];
+            if (each) each[g_off] = g;
             if (part)
-                __hip_atomic_fetch_add(part + off, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_add(part + g_off, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             return w;
         }
     }
+    __device__ __forceinline__ float with_old(int off, float g) const { return with_old(off, off, g); }
 };
 
 // Orders the LDS accesses of this wavefront's lanes around this point (a

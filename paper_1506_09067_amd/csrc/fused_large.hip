@@ -47,8 +47,26 @@ constexpr int OF1 = OB3 + C3, OBF1 = OF1 + F1 * NF1;
 constexpr int OF2 = OBF1 + F1, OBF2 = OF2 + F2 * F1;
 constexpr int NPARAM = OBF2 + F2;
 static_assert(NPARAM == 363960, "large net parameter count");
-static_assert(OW2 % 4 == 0 && KC2 % 4 == 0 && OF1 % 4 == 0 && OW3 % 4 == 0 && KC3 % 16 == 0,
-              "16-byte weight loads stay inside one row");
+
+// Device layout of the shared weights: the canonical blocks in the same
+// order, each starting on a 64-byte boundary, and the rows of conv2, FC1 and
+// FC2 padded to whole 64-byte segments (the conv1 and conv3 rows already
+// are).  The pushes are fp32 atomic adds performed at the memory side in
+// 64-byte requests; a row that starts mid-segment costs one request more per
+// 64 consecutive weights, which for the canonical FC1 and conv2 rows is 10 %
+// of the update stream.  Padding is never read or written.  get/set/update
+// convert (chaos_api.hip); gradients are produced in the canonical layout.
+constexpr int align16(int v) { return (v + 15) / 16 * 16; }
+constexpr int KC2S = 192, NF1S = 912, F1S = 160;  // padded row strides (floats)
+constexpr int DW1 = 0, DB1 = DW1 + C1 * 16;
+constexpr int DW2 = align16(DB1 + C1), DB2 = DW2 + C2 * KC2S;
+constexpr int DW3 = align16(DB2 + C2), DB3 = DW3 + C3 * KC3;
+constexpr int DF1 = align16(DB3 + C3), DBF1 = DF1 + F1 * NF1S;
+constexpr int DF2 = align16(DBF1 + F1), DBF2 = DF2 + F2 * F1S;
+constexpr int NDEV = align16(DBF2 + F2);
+static_assert(KC2S >= KC2 && NF1S >= NF1 && F1S >= F1 && KC2S % 16 == 0 && NF1S % 16 == 0 &&
+                  F1S % 16 == 0 && KC3 % 16 == 0,
+              "padded rows are whole 64-byte segments; 16-byte loads stay inside a row");
 
 constexpr int NT = 256;   // threads per worker
 constexpr int NW = NT / 64;
@@ -138,13 +156,14 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
             for (int q = 0; q < PER; ++q) {
                 const int t4 = tid + NT * q;
-                wv[q] = (t4 < N4) ? *(const f4 *)(W + OW2 + 4 * t4) : f4{0.f, 0.f, 0.f, 0.f};
+                const int o = (4 * t4) / KC2, k = 4 * t4 - o * KC2;  // KC2 % 4 == 0: one row
+                wv[q] = (t4 < N4) ? *(const f4 *)(W + DW2 + o * KC2S + k) : f4{0.f, 0.f, 0.f, 0.f};
             }
 #pragma unroll
             for (int q = 0; q < PER; ++q) {
                 const int t4 = tid + NT * q;
                 if (t4 < N4) {
-                    const int o = (4 * t4) / KC2, k = 4 * t4 - o * KC2;  // KC2 % 4 == 0: one row
+                    const int o = (4 * t4) / KC2, k = 4 * t4 - o * KC2;
 #pragma unroll
                     for (int e = 0; e < 4; ++e) sm.w2s[(k + e) * 65 + o] = wv[q][e];
                 }
@@ -165,11 +184,11 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                 for (int j = 0; j < 2; ++j) {
                     int o = 16 * j + lr;
-                    bw[s][j] = (o < C1) ? W[OW1 + o * 16 + 4 * s + lg] : 0.0f;
+                    bw[s][j] = (o < C1) ? W[DW1 + o * 16 + 4 * s + lg] : 0.0f;
                 }
             float b1[2];
 #pragma unroll
-            for (int j = 0; j < 2; ++j) b1[j] = (16 * j + lr < C1) ? W[OB1 + 16 * j + lr] : 0.0f;
+            for (int j = 0; j < 2; ++j) b1[j] = (16 * j + lr < C1) ? W[DB1 + 16 * j + lr] : 0.0f;
             // a wavefront's tiles i = wave + 4q, six at a time (12 independent
             // accumulators keep the matrix core busy)
             for (int i0 = wave; i0 < 43; i0 += 6 * NW) {
@@ -246,7 +265,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             for (int j = 0; j < 4; ++j) {
                 int o = 16 * j + lr;
                 if (o >= C2) continue;
-                float bias = W[OB2 + o];
+                float bias = W[DB2 + o];
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -285,7 +304,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     // padding columns (o >= C3) read the last map: their
                     // accumulators are never used, and no branch splits the loads
                     int o = 16 * j + lr;
-                    b[j] = *(const f4 *)(W + OW3 + (o < C3 ? o : C3 - 1) * KC3 + 16 * S + 4 * lg);
+                    b[j] = *(const f4 *)(W + DW3 + (o < C3 ? o : C3 - 1) * KC3 + 16 * S + 4 * lg);
                 }
             };
             auto compute = [&](const f4 (&b)[7], int S) {
@@ -354,7 +373,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     if ((j >= 4) != (wave == 1)) continue;
                     int o = 16 * j + lr;
                     if (o >= C3) continue;
-                    float bias = W[OB3 + o];
+                    float bias = W[DB3 + o];
 #pragma unroll
                     for (int i = 0; i < 3; ++i) {
                         f4 t = acc[i][j] + *(const f4 *)(buf + ((i * 7 + j) * 64 + lane) * 4);
@@ -394,7 +413,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                     for (int c = 0; c < 4; ++c) {
                         int j = j0 + q, i = 4 * lane + 256 * c;
-                        wv[q][c] = (j < je && i < NF1) ? *(const f4 *)(W + OF1 + j * NF1 + i)
+                        wv[q][c] = (j < je && i < NF1) ? *(const f4 *)(W + DF1 + j * NF1S + i)
                                                        : f4{0.f, 0.f, 0.f, 0.f};
                     }
             };
@@ -427,13 +446,13 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 t1 += __shfl_xor(t1, 2, 64);
                 t1 += __shfl_xor(t1, 1, 64);
                 const int j = j0 + ((lane >> 3) & 7);
-                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[OBF1 + j]);
+                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[DBF1 + j]);
             }
         }
         __syncthreads();
         // FC2 (output layer)
         for (int j = wave; j < F2; j += NW) {
-            const float *wj = W + OF2 + j * F1;
+            const float *wj = W + DF2 + j * F1S;
             float s = 0.0f;
 #pragma unroll
             for (int it = 0; it < 3; ++it) {
@@ -441,7 +460,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 if (i < F1) s = fmaf(wj[i], sm.h[i], s);
             }
             s = wave_sum(s);
-            if (lane == 0) sm.o[j] = act_y(s + W[OBF2 + j]);
+            if (lane == 0) sm.o[j] = act_y(s + W[DBF2 + j]);
         }
         __syncthreads();
         if (a.out && tid < F2) a.out[idx * F2 + tid] = sm.o[tid];
@@ -482,7 +501,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         if (tid < F1) {
             float wv[F2];
 #pragma unroll
-            for (int j = 0; j < F2; ++j) wv[j] = W[OF2 + j * F1 + tid];
+            for (int j = 0; j < F2; ++j) wv[j] = W[DF2 + j * F1S + tid];
             float s = 0.0f;
 #pragma unroll
             for (int j = 0; j < F2; ++j) s = fmaf(wv[j], sm.dout[j], s);
@@ -498,10 +517,10 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         // per input; the four partial sums are added in wavefront order.
         for (int t = tid; t < F2 * F1; t += NT) {
             int j = t / F1, i = t - j * F1;
-            push(OF2 + t, sm.dout[j] * sm.h[i]);
+            push(DF2 + j * F1S + i, OF2 + t, sm.dout[j] * sm.h[i]);
         }
-        if (tid < F2) push(OBF2 + tid, sm.dout[tid]);
-        if (tid < F1) push(OBF1 + tid, sm.dh[tid]);
+        if (tid < F2) push(DBF2 + tid, OBF2 + tid, sm.dout[tid]);
+        if (tid < F1) push(DBF1 + tid, OBF1 + tid, sm.dh[tid]);
         if constexpr (MODE == kForwardBackward) {
             // frozen weights: read them (16-byte loads, ten rows per batch,
             // the next batch requested while this one is summed), then push
@@ -511,7 +530,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 auto load = [&](f4 (&w)[10], int j0) {
 #pragma unroll
                     for (int jj = 0; jj < 10; ++jj)
-                        w[jj] = *(const f4 *)(W + OF1 + (j0 + jj) * NF1 + 4 * tid);
+                        w[jj] = *(const f4 *)(W + DF1 + (j0 + jj) * NF1S + 4 * tid);
                 };
                 auto comp = [&](const f4 (&w)[10], int j0) {
 #pragma unroll
@@ -546,7 +565,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                     for (int c = 0; c < 15; ++c) {
                         int i = lane + 64 * c;
-                        if (i < NF1) push(OF1 + j * NF1 + i, d * xv[c]);
+                        if (i < NF1) push(DF1 + j * NF1S + i, OF1 + j * NF1 + i, d * xv[c]);
                     }
                 }
             }
@@ -572,7 +591,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                             for (int c = 0; c < 15; ++c) {
                                 int i = lane + 64 * c;
-                                old[r][c] = (i < NF1) ? push.with_old(OF1 + jr * NF1 + i, dr[r] * xv[c])
+                                old[r][c] = (i < NF1) ? push.with_old(DF1 + jr * NF1S + i, OF1 + jr * NF1 + i, dr[r] * xv[c])
                                                       : 0.0f;
                             }
                         } else {
@@ -631,7 +650,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             const int arow = k0 + (lr >> 2) * 36 + (lr & 3);
             float aA[9], aB[9], bA[3], bB[3];
             auto load = [&](float (&av)[9], float (&bv)[3], int ks) {
-                const float *w3 = W + OW3 + (4 * ks + lg) * KC3 + arow;
+                const float *w3 = W + DW3 + (4 * ks + lg) * KC3 + arow;
 #pragma unroll
                 for (int i = 0; i < 9; ++i) av[i] = w3[4 * i];
                 const float *dd = sm.d3 + (4 * ks + lg) * M3P + lr;
@@ -730,13 +749,13 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                             for (int r = 0; r < 16; ++r) {
                                 const int o = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                                push(OW3 + o * KC3 + k, c32[i][kt][r]);
+                                push(DW3 + o * KC3 + k, OW3 + o * KC3 + k, c32[i][kt][r]);
                             }
                     }
                 }
                 if (k4 < KC3) {
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) push(OW3 + (96 + r) * KC3 + k4, c4[0][r] + c4[1][r]);
+                    for (int r = 0; r < 4; ++r) push(DW3 + (96 + r) * KC3 + k4, OW3 + (96 + r) * KC3 + k4, c4[0][r] + c4[1][r]);
                 }
             }
             if (tid < C3) {
@@ -744,7 +763,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 float g4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int m = 0; m < M3; ++m) g4[m & 3] += sm.d3[tid * M3P + m];
-                push(OB3 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                push(DB3 + tid, OB3 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
             }
         }
         __syncthreads();
@@ -779,7 +798,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             krow[3] = (lr < 9) ? (c0 + 4) * 9 + lr : -1;
             float aA[4], aB[4];
             auto load_a = [&](float (&av)[4], int ks) {
-                const float *w2 = W + OW2 + (4 * ks + lg) * KC2;
+                const float *w2 = W + DW2 + (4 * ks + lg) * KC2S;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) av[i] = (krow[i] >= 0) ? w2[krow[i]] : 0.0f;
             };
@@ -891,14 +910,14 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         int o = 16 * i + 4 * lg + r;
-                        if (o < C2) push(OW2 + o * KC2 + k, acc[i][j][r]);
+                        if (o < C2) push(DW2 + o * KC2S + k, OW2 + o * KC2 + k, acc[i][j][r]);
                     }
             }
             if (tid < C2) {
                 float g4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
                 for (int p = 0; p < NY2; ++p) g4[p & 3] += sm.y2[tid * NY2 + p];
-                push(OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                push(DB2 + tid, OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
             }
             for (int t = tid; t < C1 * NP1; t += NT) sm.s2[t] *= dact_from_y(sm.p1[t]);
         }
@@ -945,13 +964,13 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     float g = red[(0 * 2 + tile) * 256 + e];
 #pragma unroll
                     for (int w = 1; w < NW; ++w) g += red[(w * 2 + tile) * 256 + e];
-                    push(OW1 + t, g);
+                    push(DW1 + t, OW1 + t, g);
                 } else {
                     const int o = t - C1 * 16;
                     float g4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
                     for (int q = 0; q < NP1; ++q) g4[q & 3] += sm.s2[o * NP1 + q];
-                    push(OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                    push(DB1 + o, OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
                 }
             }
         }
@@ -961,6 +980,19 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 }
 
 } // namespace
+
+void fused_large_layout(ParamLayout &L) {
+    static const ParamSegment seg[] = {
+        {OW1, DW1, 1, C1 * 16, C1 * 16}, {OB1, DB1, 1, C1, C1},   {OW2, DW2, C2, KC2, KC2S},
+        {OB2, DB2, 1, C2, C2},           {OW3, DW3, 1, C3 * KC3, C3 * KC3},
+        {OB3, DB3, 1, C3, C3},           {OF1, DF1, F1, NF1, NF1S}, {OBF1, DBF1, 1, F1, F1},
+        {OF2, DF2, F2, F1, F1S},         {OBF2, DBF2, 1, F2, F2}};
+    constexpr int n = sizeof(seg) / sizeof(seg[0]);
+    static_assert(n <= kMaxSegments, "segment table size");
+    L.n_seg = n;
+    L.n_dev = NDEV;
+    for (int s = 0; s < n; ++s) L.seg[s] = seg[s];
+}
 
 bool fused_large_matches(const Net &net) {
     static const int spec[][3] = {{kConv, 20, 4}, {kPool, 0, 2}, {kConv, 60, 3}, {kConv, 100, 6},

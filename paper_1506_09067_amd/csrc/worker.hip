@@ -313,6 +313,37 @@ __global__ void axpy_kernel(float *__restrict__ w, const float *__restrict__ g, 
     if (i < n) w[i] = fmaf(alpha, g[i], w[i]);
 }
 
+// device index of canonical index i under layout L
+__device__ __forceinline__ int64_t dev_index(const ParamLayout &L, int64_t i) {
+    for (int s = 0; s < L.n_seg; ++s) {
+        const ParamSegment &g = L.seg[s];
+        const int64_t r0 = i - g.can_off;
+        if (r0 >= 0 && r0 < (int64_t)g.rows * g.len) {
+            const int64_t r = r0 / g.len;
+            return g.dev_off + r * g.dev_stride + (r0 - r * g.len);
+        }
+    }
+    return -1;  // not reached for i < the layout's canonical size
+}
+
+__global__ void convert_params_kernel(const float *__restrict__ src, float *__restrict__ dst,
+                                      ParamLayout L, int64_t n_can, int to_device) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n_can) return;
+    const int64_t d = dev_index(L, i);
+    if (d < 0) return;
+    if (to_device) dst[d] = src[i];
+    else dst[i] = src[d];
+}
+
+__global__ void axpy_mapped_kernel(float *__restrict__ w, const float *__restrict__ g, float alpha,
+                                   ParamLayout L, int64_t n_can) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n_can) return;
+    const int64_t d = dev_index(L, i);
+    if (d >= 0) w[d] = fmaf(alpha, g[i], w[d]);
+}
+
 inline unsigned blocks_for(int64_t n, int b) { return (unsigned)((n + b - 1) / b); }
 
 } // namespace
@@ -361,6 +392,20 @@ hipError_t launch_count(const int32_t *src, float *dst, hipStream_t s) {
 hipError_t launch_axpy(float *w, const float *g, float alpha, int64_t n, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     axpy_kernel<<<blocks_for(n, 256), 256, 0, s>>>(w, g, alpha, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_convert_params(const float *src, float *dst, const ParamLayout &L, int64_t n_can,
+                                 bool to_device, hipStream_t s) {
+    if (n_can <= 0) return hipSuccess;
+    convert_params_kernel<<<blocks_for(n_can, 256), 256, 0, s>>>(src, dst, L, n_can, to_device ? 1 : 0);
+    return hipGetLastError();
+}
+
+hipError_t launch_axpy_mapped(float *w_dev, const float *g_can, float alpha, const ParamLayout &L,
+                              int64_t n_can, hipStream_t s) {
+    if (n_can <= 0) return hipSuccess;
+    axpy_mapped_kernel<<<blocks_for(n_can, 256), 256, 0, s>>>(w_dev, g_can, alpha, L, n_can);
     return hipGetLastError();
 }
 
