@@ -76,7 +76,10 @@ typedef struct chaos_net chaos_net; /* opaque; owned by the library */
  * in_w input, allocates the shared weights on the current device and copies
  * init_params_host (n_params floats, canonical layout) into them.
  * n_params must equal the architecture's weight count (Table I "Weights"
- * summed over layers), else CHAOS_ESHAPE.  *out receives the handle. */
+ * summed over layers), else CHAOS_ESHAPE.  *out receives the handle.  The
+ * library may hold the weights on the device in a padded layout of its own
+ * (rows starting on 64-byte boundaries); every weight or gradient buffer
+ * that crosses this interface is in the canonical layout. */
 int chaos_create_net(int32_t in_h, int32_t in_w, const chaos_layer *layers, int32_t n_layers,
                      const float *init_params_host, int64_t n_params, chaos_net **out);
 

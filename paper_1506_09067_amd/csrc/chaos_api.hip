@@ -234,6 +234,11 @@ int chaos_create_net(int32_t in_h, int32_t in_w, const chaos_layer *layers, int3
     if (net->fused) {
         chaos::fused_large_layout(net->layout);
         net->padded = true;
+    } else if (net->t1) {
+        chaos::fused_t1_layout(net->layout);
+        net->padded = true;
+    } else if (net->cpcp && chaos::fused_cpcp_layout(net->cpcp, net->layout)) {
+        net->padded = true;
     } else {
         net->layout.n_seg = 1;
         net->layout.n_dev = (int)n_params;

@@ -96,12 +96,15 @@ int fused_large_blocks_per_cu();
 // Fused MFMA worker for the large net of Table I (conv20k4, max1, conv60k5,
 // max2, conv100k6, max2, FC150, FC10 on 29x29 inputs); 256 threads, no scratch.
 bool fused_t1_matches(const Net &net);
+void fused_t1_layout(ParamLayout &L);  // its padded device layout
 hipError_t launch_fused_t1(int mode, const WorkArgs &a, int grid, hipStream_t s);
 int fused_t1_blocks_per_cu();
 
 // Fused MFMA workers for the Table I small (variant 1) and medium (variant 2)
 // nets: conv C1@4x4, max2, conv C2@5x5, max3, FC F1, FC10 on 29x29 inputs.
 int fused_cpcp_variant(const Net &net);  // 0 when the net is neither
+// the variant's device layout; false (L untouched) when it is the canonical one
+bool fused_cpcp_layout(int variant, ParamLayout &L);
 hipError_t launch_fused_cpcp(int variant, int mode, const WorkArgs &a, int grid, hipStream_t s);
 int fused_cpcp_blocks_per_cu(int variant);
 

@@ -16,6 +16,8 @@
 namespace chaos {
 namespace {
 
+constexpr int pad16(bool pad, int v) { return pad ? (v + 15) / 16 * 16 : v; }
+
 template <int C1_, int C2_, int F1_>
 struct Cpcp {
     static constexpr int C1 = C1_, C2 = C2_, F1 = F1_, F2 = 10;
@@ -40,19 +42,34 @@ struct Cpcp {
     static constexpr int OF1 = OB2 + C2, OBF1 = OF1 + F1 * NF1;
     static constexpr int OF2 = OBF1 + F1, OBF2 = OF2 + F2 * F1;
     static constexpr int NPARAM = OBF2 + F2;
-    // FC1 rows read with 16-byte loads when every row start is 16-byte aligned
-    static constexpr int FC1_VEC = (OF1 % 4 == 0 && NF1 % 4 == 0) ? 4 : 1;
     // A weight vector of at most 8K floats (the small net: 25.6 KB) is copied
     // into LDS once per sample and every later weight read of the sample is
     // served from there: one round trip to memory per sample instead of one
     // per layer and pass.
     static constexpr bool STAGE = NPARAM <= 8192;
     static constexpr int NPARAM4 = (NPARAM + 3) / 4 * 4;
+    // Device layout of the shared weights.  A net whose vector is not copied
+    // whole (the medium net) starts every segment on a 64-byte boundary and
+    // pads the conv2, FC1 and FC2 rows to multiples of 16 floats (the padding
+    // stays zero), so the pushes of a row cover whole 64-byte segments; the
+    // small net keeps the canonical layout.
+    static constexpr bool PAD = !STAGE;
+    static constexpr int KC2S = pad16(PAD, KC2), NF1S = pad16(PAD, NF1), F1S = pad16(PAD, F1);
+    static constexpr int DW1 = 0, DB1 = C1 * 16;
+    static constexpr int DW2 = pad16(PAD, DB1 + C1), DB2 = DW2 + C2 * KC2S;
+    static constexpr int DF1 = pad16(PAD, DB2 + C2), DBF1 = DF1 + F1 * NF1S;
+    static constexpr int DF2 = pad16(PAD, DBF1 + F1), DBF2 = DF2 + F2 * F1S;
+    static constexpr int NDEV = pad16(PAD, DBF2 + F2);
+    static_assert(PAD || NDEV == NPARAM, "the unpadded layout is the canonical one");
+    // FC1 rows read with 16-byte loads when every row start is 16-byte aligned
+    static constexpr int FC1_VEC = (DF1 % 4 == 0 && NF1S % 4 == 0 && NF1 % 4 == 0) ? 4 : 1;
     // Otherwise the conv2 weights (80 KB for the medium net), read by the
     // conv2 forward pass and again by its backward-data pass, are copied into
-    // LDS once per sample (one worker per CU then fits).
+    // LDS once per sample (one worker per CU then fits), rows of KC2 floats.
     static constexpr int NW2 = C2 * KC2;
-    static constexpr bool STAGE2 = !STAGE && NW2 <= 20480 && OW2 % 4 == 0;
+    static constexpr bool STAGE2 = !STAGE && NW2 <= 20480 && DW2 % 4 == 0 && KC2 % 4 == 0;
+    // row stride of the conv2 weights as the kernel reads them
+    static constexpr int W2S = STAGE2 ? KC2 : KC2S;
 };
 
 constexpr int NT = 256, NW = 4;
@@ -85,7 +102,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
     const float *Wg = a.params;
     // every weight read below goes through W: the LDS copy or the shared vector
     const float *W = S::STAGE ? (const float *)sm.w : Wg;
-    const float *W2 = S::STAGE2 ? (const float *)sm.w2 : W + S::OW2;  // conv2 weights [o][k]
+    const float *W2 = S::STAGE2 ? (const float *)sm.w2 : W + S::DW2;  // conv2 weights [o][k], rows W2S apart
     constexpr bool kTrain = (MODE == kTrainAtomic || MODE == kTrainRacy);
     // the FC1 partial derivatives come from a separate read of the weights
     // (frozen weights, or the LDS copy) instead of the values returned by the
@@ -155,7 +172,8 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
             for (int q = 0; q < PER; ++q) {
                 const int t4 = tid + NT * q;
-                wv[q] = (t4 < N4) ? *(const f4 *)(Wg + S::OW2 + 4 * t4) : f4{0.f, 0.f, 0.f, 0.f};
+                const int o = 4 * t4 / S::KC2, k = 4 * t4 - o * S::KC2;  // a row holds whole 16-byte groups
+                wv[q] = (t4 < N4) ? *(const f4 *)(Wg + S::DW2 + o * S::KC2S + k) : f4{0.f, 0.f, 0.f, 0.f};
             }
             for (int i = tid; i < S::NX; i += NT) sm.x[i] = a.x[idx * S::NX + i];
 #pragma unroll
@@ -176,11 +194,11 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                 for (int j = 0; j < S::CT1; ++j) {
                     int o = 16 * j + lr;
-                    bw[s][j] = (o < S::C1) ? W[S::OW1 + o * 16 + 4 * s + lg] : 0.0f;
+                    bw[s][j] = (o < S::C1) ? W[S::DW1 + o * 16 + 4 * s + lg] : 0.0f;
                 }
             float b1[S::CT1];
 #pragma unroll
-            for (int j = 0; j < S::CT1; ++j) b1[j] = (16 * j + lr < S::C1) ? W[S::OB1 + 16 * j + lr] : 0.0f;
+            for (int j = 0; j < S::CT1; ++j) b1[j] = (16 * j + lr < S::C1) ? W[S::DB1 + 16 * j + lr] : 0.0f;
             // a wavefront's tiles i = wave + 4q, six at a time
             for (int i0 = wave; i0 < 43; i0 += 6 * NW) {
                 f4 acc[6][S::CT1];
@@ -255,7 +273,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             for (int j = 0; j < S::CT2; ++j) {
                 int o = 16 * j + lr;
                 ov[j] = o < S::C2;
-                wrow[j] = W2 + (ov[j] ? o : 0) * S::KC2 + kb;
+                wrow[j] = W2 + (ov[j] ? o : 0) * S::W2S + kb;
             }
             float bw[3][S::CT2][4];
             auto load = [&](float (&b)[S::CT2][4], int blk) {
@@ -316,7 +334,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 for (int j = 0; j < S::CT2; ++j) {
                     int o = 16 * j + lr;
                     if (o >= S::C2) continue;
-                    float bias = W[S::OB2 + o];
+                    float bias = W[S::DB2 + o];
 #pragma unroll
                     for (int i = 0; i < 3; ++i) {
                         f4 t = acc[i][j] + *(const f4 *)(red + ((i * S::CT2 + j) * 64 + lane) * 4);
@@ -377,7 +395,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     for (int c = 0; c < IC; ++c) {
                         const int j = j0 + q, i = VEC * lane + 64 * VEC * c;
                         const bool v = j < je && i < S::NF1;
-                        const float *src = W + S::OF1 + (v ? j * S::NF1 + i : 0);
+                        const float *src = W + S::DF1 + (v ? j * S::NF1S + i : 0);
                         if (VEC == 4) {
                             f4 t = v ? *(const f4 *)src : f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -413,7 +431,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 t1 += __shfl_xor(t1, 2, 64);
                 t1 += __shfl_xor(t1, 1, 64);
                 const int j = j0 + ((lane >> 3) & 7);
-                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[S::OBF1 + j]);
+                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[S::DBF1 + j]);
             }
         }
         __syncthreads();
@@ -422,10 +440,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
             for (int it = 0; it < (S::F1 + 63) / 64; ++it) {
                 int i = lane + 64 * it;
-                if (i < S::F1) s = fmaf(W[S::OF2 + j * S::F1 + i], sm.h[i], s);
+                if (i < S::F1) s = fmaf(W[S::DF2 + j * S::F1S + i], sm.h[i], s);
             }
             s = wave_sum(s);
-            if (lane == 0) sm.o[j] = act_y(s + W[S::OBF2 + j]);
+            if (lane == 0) sm.o[j] = act_y(s + W[S::DBF2 + j]);
         }
         __syncthreads();
         if (a.out && tid < S::F2) a.out[idx * S::F2 + tid] = sm.o[tid];
@@ -465,7 +483,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         for (int i = tid; i < S::F1; i += NT) {
             float wv[S::F2];
 #pragma unroll
-            for (int j = 0; j < S::F2; ++j) wv[j] = W[S::OF2 + j * S::F1 + i];
+            for (int j = 0; j < S::F2; ++j) wv[j] = W[S::DF2 + j * S::F1S + i];
             float s = 0.0f;
 #pragma unroll
             for (int j = 0; j < S::F2; ++j) s = fmaf(wv[j], sm.dout[j], s);
@@ -475,9 +493,9 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         // FC2 push; FC1 push and FC1 backward data
         for (int t = tid; t < S::F2 * S::F1; t += NT) {
             int j = t / S::F1, i = t - j * S::F1;
-            push(S::OF2 + t, sm.dout[j] * sm.h[i]);
+            push(S::DF2 + j * S::F1S + i, S::OF2 + t, sm.dout[j] * sm.h[i]);
         }
-        if (tid < S::F2) push(S::OBF2 + tid, sm.dout[tid]);
+        if (tid < S::F2) push(S::DBF2 + tid, S::OBF2 + tid, sm.dout[tid]);
         if constexpr (kFc1Read) {
             // read the weights (frozen, or this sample's LDS copy), then push
             // FC1 backward data (pre-update weights), summed over the rows in
@@ -499,7 +517,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                         for (int jj = 0; jj < 10; ++jj) {
                             const int j = j0 + jj;
-                            const float *src = W + S::OF1 + (j < r1 ? j : r0) * S::NF1 + i0;
+                            const float *src = W + S::DF1 + (j < r1 ? j : r0) * S::NF1S + i0;
                             if (VEC == 4) {
                                 f4 t = *(const f4 *)src;
 #pragma unroll
@@ -549,11 +567,11 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                     for (int c = 0; c < IC; ++c) {
                         int i = lane + 64 * c;
-                        if (i < S::NF1) push(S::OF1 + j * S::NF1 + i, d * xv[c]);
+                        if (i < S::NF1) push(S::DF1 + j * S::NF1S + i, S::OF1 + j * S::NF1 + i, d * xv[c]);
                     }
                 }
             }
-            if (tid < S::F1) push(S::OBF1 + tid, sm.dh[tid]);
+            if (tid < S::F1) push(S::DBF1 + tid, S::OBF1 + tid, sm.dh[tid]);
         } else {
             // One pass: each FC1 push returns the weight it updated, this
             // layer's pre-update weight (Section III-A.2), so the errors
@@ -584,7 +602,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                         for (int c = 0; c < IC; ++c) {
                             int i = lane + 64 * c;
-                            old[r][c] = (i < S::NF1) ? push.with_old(S::OF1 + jr * S::NF1 + i, dr[r] * xv[c])
+                            old[r][c] = (i < S::NF1) ? push.with_old(S::DF1 + jr * S::NF1S + i, S::OF1 + jr * S::NF1 + i, dr[r] * xv[c])
                                                      : 0.0f;
                         }
                     } else {
@@ -602,7 +620,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 int i = lane + 64 * c;
                 if (i < S::NF1) sm.y2[wave * S::NF1 + i] = ep[c];
             }
-            if (tid < S::F1) push(S::OBF1 + tid, sm.dh[tid]);
+            if (tid < S::F1) push(S::DBF1 + tid, S::OBF1 + tid, sm.dh[tid]);
         }
         __syncthreads();
         // pool2 backward -> dense conv2 deltas; clear e1
@@ -642,7 +660,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             float aA[2], aB[2];
             auto load_a = [&](float (&av)[2], int ks) {
                 const int o = 4 * ks + lg;
-                const float *w2 = W2 + (o < S::C2 ? o : 0) * S::KC2 + c * 25;
+                const float *w2 = W2 + (o < S::C2 ? o : 0) * S::W2S + c * 25;
 #pragma unroll
                 for (int t = 0; t < 2; ++t) {
                     const int uv = 16 * t + lr;
@@ -724,7 +742,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     float aA[TI], aB[TI];
                     auto load_a = [&](float (&av)[TI], int ks) {
                         const int o = 4 * ks + lg;
-                        const float *w2 = W2 + (o < S::C2 ? o : 0) * S::KC2;
+                        const float *w2 = W2 + (o < S::C2 ? o : 0) * S::W2S;
 #pragma unroll
                         for (int t = 0; t < TI; ++t) av[t] = (o < S::C2 && wo[t] >= 0) ? w2[wo[t]] : 0.0f;
                     };
@@ -833,7 +851,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
                             int o = 16 * i + 4 * lg + r;
-                            if (o < S::C2) push(S::OW2 + o * S::KC2 + k, acc[b][i][r]);
+                            if (o < S::C2) push(S::DW2 + o * S::KC2S + k, S::OW2 + o * S::KC2 + k, acc[b][i][r]);
                         }
                 }
             }
@@ -841,7 +859,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 float g4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
                 for (int p = 0; p < S::NY2; ++p) g4[p & 3] += sm.d2[tid * 96 + p];
-                push(S::OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                push(S::DB2 + tid, S::OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
             }
             for (int t = tid; t < S::C1 * S::NP1; t += NT) sm.e1[t] *= dact_from_y(sm.p1[t]);
         }
@@ -895,13 +913,13 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     float g = red[(0 * S::CT1 + tile) * 256 + e];
 #pragma unroll
                     for (int w = 1; w < NW; ++w) g += red[(w * S::CT1 + tile) * 256 + e];
-                    push(S::OW1 + t, g);
+                    push(S::DW1 + t, S::OW1 + t, g);
                 } else {
                     const int o = t - S::C1 * 16;
                     float g4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
                     for (int q = 0; q < S::NP1; ++q) g4[q & 3] += sm.e1[o * S::NP1 + q];
-                    push(S::OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                    push(S::DB1 + o, S::OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
                 }
             }
         }
@@ -964,6 +982,30 @@ int fused_cpcp_variant(const Net &net) {
     if (matches(net, Small::C1, Small::C2, Small::F1)) return 1;
     if (matches(net, Medium::C1, Medium::C2, Medium::F1)) return 2;
     return 0;
+}
+
+namespace {
+template <class S>
+bool cpcp_layout(ParamLayout &L) {
+    if (!S::PAD) return false;
+    const ParamSegment seg[] = {
+        {S::OW1, S::DW1, 1, S::C1 * 16, S::C1 * 16}, {S::OB1, S::DB1, 1, S::C1, S::C1},
+        {S::OW2, S::DW2, S::C2, S::KC2, S::KC2S},    {S::OB2, S::DB2, 1, S::C2, S::C2},
+        {S::OF1, S::DF1, S::F1, S::NF1, S::NF1S},    {S::OBF1, S::DBF1, 1, S::F1, S::F1},
+        {S::OF2, S::DF2, S::F2, S::F1, S::F1S},      {S::OBF2, S::DBF2, 1, S::F2, S::F2}};
+    constexpr int n = sizeof(seg) / sizeof(seg[0]);
+    static_assert(n <= kMaxSegments, "segment table size");
+    L.n_seg = n;
+    L.n_dev = S::NDEV;
+    for (int s = 0; s < n; ++s) L.seg[s] = seg[s];
+    return true;
+}
+} // namespace
+
+bool fused_cpcp_layout(int variant, ParamLayout &L) {
+    if (variant == 1) return cpcp_layout<Small>(L);
+    if (variant == 2) return cpcp_layout<Medium>(L);
+    return false;
 }
 
 hipError_t launch_fused_cpcp(int variant, int mode, const WorkArgs &a, int grid, hipStream_t s) {

@@ -46,8 +46,20 @@ constexpr int OF1 = OB3 + C3, OBF1 = OF1 + F1 * NF1;
 constexpr int OF2 = OBF1 + F1, OBF2 = OF2 + F2 * F1;
 constexpr int NPARAM = OBF2 + F2;
 static_assert(NPARAM == 383160, "Table I large net weight count");
-static_assert(OW2 % 4 == 0 && KC2 % 4 == 0 && OF1 % 4 == 0 && OW3 % 4 == 0 && KC3 % 16 == 0,
-              "16-byte weight loads stay inside one row");
+
+// device layout of the shared weights: every segment starts on a 64-byte
+// boundary and the conv2, FC1 and FC2 rows are padded to multiples of 16
+// floats, so a wavefront's push of 64 consecutive weights of a row touches
+// four 64-byte segments, not five (the padding stays zero)
+constexpr int align16(int v) { return (v + 15) / 16 * 16; }
+constexpr int KC2S = align16(KC2), NF1S = align16(NF1), F1S = align16(F1);  // 512, 912, 160
+constexpr int DW1 = 0, DB1 = DW1 + C1 * 16;
+constexpr int DW2 = align16(DB1 + C1), DB2 = DW2 + C2 * KC2S;
+constexpr int DW3 = align16(DB2 + C2), DB3 = DW3 + C3 * KC3;
+constexpr int DF1 = align16(DB3 + C3), DBF1 = DF1 + F1 * NF1S;
+constexpr int DF2 = align16(DBF1 + F1), DBF2 = DF2 + F2 * F1S;
+constexpr int NDEV = align16(DBF2 + F2);
+static_assert(KC2S == KC2P && KC3 % 16 == 0, "16-byte weight loads stay inside one row");
 
 constexpr int NT = 256;   // threads per worker
 constexpr int NW = NT / 64;
@@ -143,10 +155,10 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
 #pragma unroll
                 for (int j = 0; j < 2; ++j) {
                     int o = 16 * j + lr;
-                    bw[s][j] = (o < C1) ? W[OW1 + o * 16 + 4 * s + lg] : 0.0f;
+                    bw[s][j] = (o < C1) ? W[DW1 + o * 16 + 4 * s + lg] : 0.0f;
                 }
 #pragma unroll
-            for (int j = 0; j < 2; ++j) b1[j] = (16 * j + lr < C1) ? W[OB1 + 16 * j + lr] : 0.0f;
+            for (int j = 0; j < 2; ++j) b1[j] = (16 * j + lr < C1) ? W[DB1 + 16 * j + lr] : 0.0f;
             for (int i0 = wave; i0 < 43; i0 += 6 * NW) {
                 f4 acc[6][2];
                 int base[6];
@@ -194,7 +206,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         {
             const int o = 16 * wave + lr;
             const bool ov = o < C2;
-            const float *wrow = W + OW2 + (ov ? o : 0) * KC2 + 4 * lg;
+            const float *wrow = W + DW2 + (ov ? o : 0) * KC2S + 4 * lg;
             int base[M2T];
 #pragma unroll
             for (int i = 0; i < M2T; ++i) {
@@ -248,7 +260,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 step(b3, S + 3);
             }
             if (ov) {
-                const float bias = W[OB2 + o];
+                const float bias = W[DB2 + o];
 #pragma unroll
                 for (int i = 0; i < M2T; ++i) {
                     const int P = 4 * i + lg;
@@ -291,7 +303,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     // padding columns (o >= C3) read the last map: their
                     // accumulators are never used, and no branch splits the loads
                     int o = 16 * j + lr;
-                    b[j] = *(const f4 *)(W + OW3 + (o < C3 ? o : C3 - 1) * KC3 + 16 * S + 4 * lg);
+                    b[j] = *(const f4 *)(W + DW3 + (o < C3 ? o : C3 - 1) * KC3 + 16 * S + 4 * lg);
                 }
             };
             auto compute = [&](const f4 (&b)[7], int S) {
@@ -360,7 +372,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     if ((j >= 4) != (wave == 1)) continue;
                     int o = 16 * j + lr;
                     if (o >= C3) continue;
-                    float bias = W[OB3 + o];
+                    float bias = W[DB3 + o];
 #pragma unroll
                     for (int i = 0; i < 3; ++i) {
                         f4 t = acc[i][j] + *(const f4 *)(buf + ((i * 7 + j) * 64 + lane) * 4);
@@ -400,7 +412,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
 #pragma unroll
                     for (int c = 0; c < 4; ++c) {
                         int j = j0 + q, i = 4 * lane + 256 * c;
-                        wv[q][c] = (j < je && i < NF1) ? *(const f4 *)(W + OF1 + j * NF1 + i)
+                        wv[q][c] = (j < je && i < NF1) ? *(const f4 *)(W + DF1 + j * NF1S + i)
                                                        : f4{0.f, 0.f, 0.f, 0.f};
                     }
             };
@@ -433,13 +445,13 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 t1 += __shfl_xor(t1, 2, 64);
                 t1 += __shfl_xor(t1, 1, 64);
                 const int j = j0 + ((lane >> 3) & 7);
-                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[OBF1 + j]);
+                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[DBF1 + j]);
             }
         }
         __syncthreads();
         // FC2 (output layer)
         for (int j = wave; j < F2; j += NW) {
-            const float *wj = W + OF2 + j * F1;
+            const float *wj = W + DF2 + j * F1S;
             float s = 0.0f;
 #pragma unroll
             for (int it = 0; it < 3; ++it) {
@@ -447,7 +459,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 if (i < F1) s = fmaf(wj[i], sm.h[i], s);
             }
             s = wave_sum(s);
-            if (lane == 0) sm.o[j] = act_y(s + W[OBF2 + j]);
+            if (lane == 0) sm.o[j] = act_y(s + W[DBF2 + j]);
         }
         __syncthreads();
         if (a.out && tid < F2) a.out[idx * F2 + tid] = sm.o[tid];
@@ -488,7 +500,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         if (tid < F1) {
             float wv[F2];
 #pragma unroll
-            for (int j = 0; j < F2; ++j) wv[j] = W[OF2 + j * F1 + tid];
+            for (int j = 0; j < F2; ++j) wv[j] = W[DF2 + j * F1S + tid];
             float s = 0.0f;
 #pragma unroll
             for (int j = 0; j < F2; ++j) s = fmaf(wv[j], sm.dout[j], s);
@@ -504,10 +516,10 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         // per input; the four partial sums are added in wavefront order.
         for (int t = tid; t < F2 * F1; t += NT) {
             int j = t / F1, i = t - j * F1;
-            push(OF2 + t, sm.dout[j] * sm.h[i]);
+            push(DF2 + j * F1S + i, OF2 + t, sm.dout[j] * sm.h[i]);
         }
-        if (tid < F2) push(OBF2 + tid, sm.dout[tid]);
-        if (tid < F1) push(OBF1 + tid, sm.dh[tid]);
+        if (tid < F2) push(DBF2 + tid, OBF2 + tid, sm.dout[tid]);
+        if (tid < F1) push(DBF1 + tid, OBF1 + tid, sm.dh[tid]);
         if constexpr (MODE == kForwardBackward) {
             // frozen weights: read them (16-byte loads, ten rows per batch,
             // the next batch requested while this one is summed), then push
@@ -517,7 +529,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 auto load = [&](f4 (&w)[10], int j0) {
 #pragma unroll
                     for (int jj = 0; jj < 10; ++jj)
-                        w[jj] = *(const f4 *)(W + OF1 + (j0 + jj) * NF1 + 4 * tid);
+                        w[jj] = *(const f4 *)(W + DF1 + (j0 + jj) * NF1S + 4 * tid);
                 };
                 auto comp = [&](const f4 (&w)[10], int j0) {
 #pragma unroll
@@ -552,7 +564,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
 #pragma unroll
                     for (int c = 0; c < 15; ++c) {
                         int i = lane + 64 * c;
-                        if (i < NF1) push(OF1 + j * NF1 + i, d * xv[c]);
+                        if (i < NF1) push(DF1 + j * NF1S + i, OF1 + j * NF1 + i, d * xv[c]);
                     }
                 }
             }
@@ -578,7 +590,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
 #pragma unroll
                             for (int c = 0; c < 15; ++c) {
                                 int i = lane + 64 * c;
-                                old[r][c] = (i < NF1) ? push.with_old(OF1 + jr * NF1 + i, dr[r] * xv[c])
+                                old[r][c] = (i < NF1) ? push.with_old(DF1 + jr * NF1S + i, OF1 + jr * NF1 + i, dr[r] * xv[c])
                                                       : 0.0f;
                             }
                         } else {
@@ -637,7 +649,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
             const int arow = k0 + (lr >> 2) * 36 + (lr & 3);
             float aA[9], aB[9], bA[3], bB[3];
             auto load = [&](float (&av)[9], float (&bv)[3], int ks) {
-                const float *w3 = W + OW3 + (4 * ks + lg) * KC3 + arow;
+                const float *w3 = W + DW3 + (4 * ks + lg) * KC3 + arow;
 #pragma unroll
                 for (int i = 0; i < 9; ++i) av[i] = w3[4 * i];
                 const float *dd = sm.d3 + (4 * ks + lg) * M3P + lr;
@@ -736,13 +748,13 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
 #pragma unroll
                             for (int r = 0; r < 16; ++r) {
                                 const int o = 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                                push(OW3 + o * KC3 + k, c32[i][kt][r]);
+                                push(DW3 + o * KC3 + k, OW3 + o * KC3 + k, c32[i][kt][r]);
                             }
                     }
                 }
                 if (k4 < KC3) {
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) push(OW3 + (96 + r) * KC3 + k4, c4[0][r] + c4[1][r]);
+                    for (int r = 0; r < 4; ++r) push(DW3 + (96 + r) * KC3 + k4, OW3 + (96 + r) * KC3 + k4, c4[0][r] + c4[1][r]);
                 }
             }
             if (tid < C3) {
@@ -750,7 +762,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 float g4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int m = 0; m < M3; ++m) g4[m & 3] += sm.d3[tid * M3P + m];
-                push(OB3 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                push(DB3 + tid, OB3 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
             }
         }
         __syncthreads();
@@ -787,7 +799,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
             // a select: no branch between a load and its use)
 #pragma unroll
             for (int ks = 0; ks < 15; ++ks) {
-                const float *w2 = W + OW2 + (4 * ks + lg) * KC2 + (c0 + (lr >> 2)) * 25 + (lr & 3);
+                const float *w2 = W + DW2 + (4 * ks + lg) * KC2S + (c0 + (lr >> 2)) * 25 + (lr & 3);
 #pragma unroll
                 for (int i = 0; i < 7; ++i) {
                     const bool ok = 4 * i + (lr & 3) < 25;
@@ -908,7 +920,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
                         const int o = 16 * i + 4 * lg + r;
-                        if (o < C2) push(OW2 + o * KC2 + k, acc[i][q][r]);
+                        if (o < C2) push(DW2 + o * KC2S + k, OW2 + o * KC2 + k, acc[i][q][r]);
                     }
             }
         };
@@ -923,7 +935,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 float g4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
                 for (int P = 0; P < NY2; ++P) g4[P & 3] += sm.y2[tid * NY2 + P];
-                push(OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                push(DB2 + tid, OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
             }
         }
         __syncthreads();
@@ -970,13 +982,13 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     float g = sm.red1[(0 * 2 + tile) * 256 + e];
 #pragma unroll
                     for (int w = 1; w < NW; ++w) g += sm.red1[(w * 2 + tile) * 256 + e];
-                    push(OW1 + t, g);
+                    push(DW1 + t, OW1 + t, g);
                 } else {
                     const int o = t - C1 * 16;
                     float g4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
                     for (int q = 0; q < NA1; ++q) g4[q & 3] += sm.e1[o * NA1 + q];
-                    push(OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                    push(DB1 + o, OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
                 }
             }
         }
@@ -998,6 +1010,19 @@ bool fused_t1_matches(const Net &net) {
         if (ly.kind != kPool && ly.cout != spec[l][1]) return false;
     }
     return net.L[0].hin == IN && net.L[0].win == IN;
+}
+
+void fused_t1_layout(ParamLayout &L) {
+    static const ParamSegment seg[] = {
+        {OW1, DW1, 1, C1 * 16, C1 * 16}, {OB1, DB1, 1, C1, C1},   {OW2, DW2, C2, KC2, KC2S},
+        {OB2, DB2, 1, C2, C2},           {OW3, DW3, 1, C3 * KC3, C3 * KC3},
+        {OB3, DB3, 1, C3, C3},           {OF1, DF1, F1, NF1, NF1S}, {OBF1, DBF1, 1, F1, F1},
+        {OF2, DF2, F2, F1, F1S},         {OBF2, DBF2, 1, F2, F2}};
+    constexpr int n = sizeof(seg) / sizeof(seg[0]);
+    static_assert(n <= kMaxSegments, "segment table size");
+    L.n_seg = n;
+    L.n_dev = NDEV;
+    for (int s = 0; s < n; ++s) L.seg[s] = seg[s];
 }
 
 hipError_t launch_fused_t1(int mode, const WorkArgs &a, int grid, hipStream_t s) {

@@ -246,10 +246,10 @@ def test_bad_arguments_are_rejected(chaos, torch_cuda):
     assert e.value.code == chaos.EINVAL
 
 
-@pytest.mark.parametrize("name", ["medium", "large"])
+@pytest.mark.parametrize("name", ["medium", "large", "large_table1"])
 def test_apply_update_and_param_roundtrip(chaos, torch_cuda, name):
-    # the large net keeps its weights in a padded device layout: get, set
-    # and update convert, so the canonical view must round-trip exactly
+    # the two large nets keep their weights in a padded device layout: get,
+    # set and update convert, so the canonical view must round-trip exactly
     torch = torch_cuda
     net, _, p = _net(chaos, name)
     g = torch.randn(net.n_params, device="cuda")
@@ -354,7 +354,7 @@ def test_train_session_equals_manual_epochs(chaos, torch_cuda):
     assert st[-1, 0] < st[0, 0]  # training loss goes down over the epochs
 
 
-@pytest.mark.parametrize("name", ["small", "large"])
+@pytest.mark.parametrize("name", ["small", "large", "large_table1"])
 def test_one_wavefront_workers_beyond_the_fused_capacity(chaos, torch_cuda, name):
     """Worker counts above chaos_max_workers run one-wavefront generic workers:
     every sample is claimed once, lr = 0 leaves the weights unchanged and the
