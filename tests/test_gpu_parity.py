@@ -156,6 +156,30 @@ def test_sequential_sgd_tiny_run(chaos, torch_cuda):
         assert norm <= 1e-3, f"weights after 1000 samples ({amb.size} ambiguous): {msg}"
 
 
+@pytest.mark.parametrize("name,n", [("medium", 40), ("large", 24), ("large_table1", 16)])
+def test_sequential_sgd_short_run(chaos, torch_cuda, name, n):
+    """Per-sample SGD on the nets whose weights the library pads on the
+    device, against the oracle: per-sample losses and final weights (the
+    canonical view), up to the first sample with an ambiguous max-pool tie."""
+    torch = torch_cuda
+    layers = wl.NETS[name]
+    p = wl.init_params(layers)
+    x, y = wl.tiny_set(n)
+    _, _, gaps = orc.train_sequential(layers, p, x, y, 1e-3, with_gaps=True)
+    amb = np.where(gaps < AMBIGUOUS)[0]
+    n_cut = int(amb[0]) if amb.size else n
+    assert n_cut >= 8
+    net, _, _ = _net(chaos, name)
+    loss = torch.empty(n_cut, device="cuda")
+    net.train_epoch(_dev(torch, x[:n_cut], torch.float32), _dev(torch, y[:n_cut], torch.int32), 1e-3,
+                    mode=chaos.SEQUENTIAL, loss=loss)
+    w = net.get_params().cpu().numpy()
+    p_ref, L_ref = orc.train_sequential(layers, p, x[:n_cut], y[:n_cut], 1e-3)
+    assert_close(loss.cpu().numpy(), L_ref, what=f"per-sample losses, {n_cut} samples")
+    assert_close(w, p_ref, what=f"weights after {n_cut} samples")
+    assert_close(w - p, p_ref - p, tol=1e-3, what="total weight change")
+
+
 @pytest.mark.parametrize("name", ["small", "medium", "large", "large_table1"])
 def test_hogwild_one_worker_is_sequential(chaos, torch_cuda, name):
     torch = torch_cuda
@@ -201,9 +225,10 @@ def test_lr_zero_and_claims_once(chaos, torch_cuda, mode, name):
     assert torch.equal(loss, ref_loss)
 
 
-def test_evaluate_matches_oracle(chaos, torch_cuda):
+@pytest.mark.parametrize("name", ["small", "medium", "large", "large_table1"])
+def test_evaluate_matches_oracle(chaos, torch_cuda, name):
     torch = torch_cuda
-    net, layers, p = _net(chaos, "large")
+    net, layers, p = _net(chaos, name)
     n = 64
     x, y = wl.test_set(n)
     out = torch.empty(n, net.n_out, device="cuda")
@@ -214,9 +239,10 @@ def test_evaluate_matches_oracle(chaos, torch_cuda):
     assert int(wrong.item()) == ref_wrong
 
 
-def test_empty_and_single_inputs(chaos, torch_cuda):
+@pytest.mark.parametrize("name", ["small", "medium", "large", "large_table1"])
+def test_empty_and_single_inputs(chaos, torch_cuda, name):
     torch = torch_cuda
-    net, layers, p = _net(chaos, "small")
+    net, layers, p = _net(chaos, name)
     x0 = torch.empty(0, 841, device="cuda")
     y0 = torch.empty(0, dtype=torch.int32, device="cuda")
     g = torch.full((net.n_params,), 7.0, device="cuda")
