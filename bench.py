@@ -132,6 +132,41 @@ def cpu_baseline(layers, p0, x, y, budget_s=15.0):
                       f"per-sample SGD (fp64 oracle, one thread), {dt:.1f} s"}
 
 
+def cpu_batch_baseline(layers, p0, x, y, budget_s=3.0):
+    """The oracle's frozen-weight gradient sum on every host core the process
+    may use (at most 16): contiguous chunks of a prefix of the batch, one
+    thread each (the oracle's C call releases the interpreter lock), partial
+    sums added in chunk order."""
+    import threading
+    import numpy as np
+    from oracle import oracle as orc
+    cores = max(1, min(len(os.sched_getaffinity(0)), int(os.environ.get("OMP_NUM_THREADS", 16)), 16))
+    t0 = time.perf_counter()
+    orc.grad_sum(layers, p0, x[:2], y[:2])
+    per = (time.perf_counter() - t0) / 2
+    k = max(1, min(len(y) // cores, int(budget_s / max(per, 1e-6))))
+    n = k * cores
+    parts = [None] * cores
+
+    def work(t):
+        parts[t] = orc.grad_sum(layers, p0, x[t * k:(t + 1) * k], y[t * k:(t + 1) * k])[0]
+
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(cores)]
+    t0 = time.perf_counter()
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    g = np.zeros_like(parts[0])
+    for q in parts:
+        g += q
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "samples/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {n} samples of the 16,384-sample batch, frozen-weight gradient "
+                      f"sum (fp64 oracle, {cores} threads of {k} samples, partial sums added "
+                      f"in order), {dt:.1f} s"}
+
+
 def train_row(chaos, wl, torch, name, xd, yd, x, y, steps, with_cpu):
     """Training throughput of one net over the resident training set with
     every resident worker (atomic pushes, lr 1e-3)."""
@@ -415,6 +450,8 @@ def main():
         torch.cuda.synchronize()
         rows["batch_gradient_16384"] = {"samples_per_s": 16384 / (a.elapsed_time(b) / 1e3),
                                         "ms": a.elapsed_time(b)}
+        if not args.no_cpu_baseline:
+            rows["batch_gradient_16384"]["cpu_oracle"] = cpu_batch_baseline(layers, p0, xb, yb)
         xt, yt = wl.test_set(10000)
         xtd, ytd = torch.from_numpy(xt).cuda(), torch.from_numpy(yt).cuda()
         net.evaluate(xtd, ytd)

@@ -148,6 +148,9 @@ int chaos_evaluate(chaos_net *net, const float *x_dev, const int32_t *labels_dev
  *   [1] wrong predictions on the training set after the epoch (Validation)
  *   [2] wrong predictions on the test set (Testing, the Table II count)
  *   [3] mean test loss
+ * ckpt_dev (optional, NULL = skip) [epochs][n_params] receives the weights
+ * after each epoch's Training, canonical layout: the per-epoch serialization
+ * of intermediate results of the paper's time model (Section III-B, term d).
  * n_test may be 0 (then [2] and [3] are 0).  Uses net-owned buffers of
  * n_train and n_test floats, allocated on first use (the only call here that
  * may allocate device memory after chaos_create_net, together with the batch
@@ -155,7 +158,7 @@ int chaos_evaluate(chaos_net *net, const float *x_dev, const int32_t *labels_dev
 int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t *labels_train_dev,
                         int64_t n_train, const float *x_test_dev, const int32_t *labels_test_dev,
                         int64_t n_test, int32_t epochs, float lr0, float decay, int32_t mode,
-                        int32_t workers, float *stats_dev, hipStream_t stream);
+                        int32_t workers, float *stats_dev, float *ckpt_dev, hipStream_t stream);
 
 /* Concurrent Hogwild workers the net's own kernel keeps resident (the
  * default worker count). */

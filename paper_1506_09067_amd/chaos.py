@@ -58,7 +58,7 @@ def lib():
             "chaos_apply_update": ([P, P, f32, P], ctypes.c_int),
             "chaos_train_epoch": ([P, P, P, i64, f32, i32, i32, P, P], ctypes.c_int),
             "chaos_evaluate": ([P, P, P, i64, P, P, P], ctypes.c_int),
-            "chaos_train_session": ([P, P, P, i64, P, P, i64, i32, f32, f32, i32, i32, P, P],
+            "chaos_train_session": ([P, P, P, i64, P, P, i64, i32, f32, f32, i32, i32, P, P, P],
                                     ctypes.c_int),
             "chaos_max_workers": ([P], ctypes.c_int32),
             "chaos_worker_limit": ([P], ctypes.c_int32),
@@ -181,16 +181,20 @@ class Net:
                                        _dev(loss, torch.float32, "loss", n, True), _stream()))
 
     def train_session(self, x, labels, x_test, labels_test, epochs: int, lr0: float,
-                      decay: float = 1.0, mode: int = HOGWILD_ATOMIC, workers: int = 0):
+                      decay: float = 1.0, mode: int = HOGWILD_ATOMIC, workers: int = 0,
+                      checkpoints=None):
         """Training + Validation + Testing per epoch; returns stats [epochs][4] on
         the device: mean training loss, wrong on the training set, wrong on the
-        test set, mean test loss."""
+        test set, mean test loss.  checkpoints: optional float32 CUDA tensor
+        [epochs][n_params] that receives the weights after each epoch's
+        Training (canonical layout)."""
         px, py, n = self._xy(x, labels)
         pxt, pyt, nt = self._xy(x_test, labels_test)
         stats = torch.empty(max(epochs, 1), 4, dtype=torch.float32, device="cuda")
+        ck = _dev(checkpoints, torch.float32, "checkpoints", max(epochs, 0) * self.n_params, True)
         _check(lib().chaos_train_session(self._h, px, py, n, pxt, pyt, nt, int(epochs),
                                          float(lr0), float(decay), int(mode), int(workers),
-                                         ctypes.c_void_p(stats.data_ptr()), _stream()))
+                                         ctypes.c_void_p(stats.data_ptr()), ck, _stream()))
         return stats[:epochs]
 
     def evaluate(self, x, labels, out=None, n_wrong=None):

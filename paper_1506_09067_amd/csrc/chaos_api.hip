@@ -466,7 +466,7 @@ int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *la
 int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t *labels_train_dev,
                         int64_t n_train, const float *x_test_dev, const int32_t *labels_test_dev,
                         int64_t n_test, int32_t epochs, float lr0, float decay, int32_t mode,
-                        int32_t workers, float *stats_dev, hipStream_t stream) {
+                        int32_t workers, float *stats_dev, float *ckpt_dev, hipStream_t stream) {
     if (int rc = check_net(net)) return rc;
     if (int rc = check_io(x_train_dev, labels_train_dev, n_train)) return rc;
     if (int rc = check_io(x_test_dev, labels_test_dev, n_test)) return rc;
@@ -479,8 +479,7 @@ int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t 
     if (int rc = set_device(net)) return rc;
     const int64_t need = std::max<int64_t>(std::max(n_train, n_test), 1);
     if (need > net->sess_loss_n) {
-        (void)hipFree(net->wide_scratch);
-    (void)hipFree(net->sess_loss);
+        (void)hipFree(net->sess_loss);
         net->sess_loss = nullptr;
         net->sess_loss_n = 0;
         if (hipMalloc(&net->sess_loss, (size_t)need * sizeof(float)) != hipSuccess)
@@ -495,6 +494,8 @@ int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t 
         int rc = chaos_train_epoch(net, x_train_dev, labels_train_dev, n_train, lr, mode, workers,
                                    n_train ? net->sess_loss : nullptr, stream);
         if (rc) return rc;
+        if (ckpt_dev && (rc = chaos_get_params(net, ckpt_dev + (int64_t)e * net->n_params, stream)))
+            return rc;
         HIP_TRY(chaos::launch_mean(net->sess_loss, n_train, st + 0, stream), "session mean");
         if ((rc = chaos_evaluate(net, x_train_dev, labels_train_dev, n_train, nullptr,
                                  net->sess_wrong, stream)))

@@ -347,7 +347,8 @@ def test_full_size_hogwild_epoch(chaos, torch_cuda):
     assert not torch.equal(w.cpu(), torch.from_numpy(p))
 
 
-def test_train_session_equals_manual_epochs(chaos, torch_cuda):
+@pytest.mark.parametrize("name", ["small", "medium"])
+def test_train_session_equals_manual_epochs(chaos, torch_cuda, name):
     """The per-epoch driver (Training, Validation on the training set, Testing)
     equals the same calls made one by one; sequential mode, lr decaying."""
     torch = torch_cuda
@@ -356,16 +357,19 @@ def test_train_session_equals_manual_epochs(chaos, torch_cuda):
     xd, yd = _dev(torch, x, torch.float32), _dev(torch, y, torch.int32)
     xtd, ytd = _dev(torch, xt, torch.float32), _dev(torch, yt, torch.int32)
     lr0, decay, epochs = 1e-2, 0.9, 3
-    net, _, p = _net(chaos, "small")
-    stats = net.train_session(xd, yd, xtd, ytd, epochs, lr0, decay, mode=chaos.SEQUENTIAL)
+    net, _, p = _net(chaos, name)
+    ckpt = torch.empty(epochs, net.n_params, device="cuda")
+    stats = net.train_session(xd, yd, xtd, ytd, epochs, lr0, decay, mode=chaos.SEQUENTIAL,
+                              checkpoints=ckpt)
     w_session = net.get_params()
-    ref, _, _ = _net(chaos, "small")
+    ref, _, _ = _net(chaos, name)
     lr0f, decayf = float(np.float32(lr0)), float(np.float32(decay))
     rows = []
     for e in range(epochs):
         lr = float(np.float32(lr0f * decayf ** e))
         loss = torch.empty(500, device="cuda")
         ref.train_epoch(xd, yd, lr, mode=chaos.SEQUENTIAL, loss=loss)
+        assert torch.equal(ckpt[e], ref.get_params())  # the epoch's checkpoint
         w_train = int(ref.evaluate(xd, yd).item())
         w_test = int(ref.evaluate(xtd, ytd).item())
         tl = torch.empty(300, device="cuda")
@@ -378,6 +382,38 @@ def test_train_session_equals_manual_epochs(chaos, torch_cuda):
         assert abs(st[e, 0] - ml) <= 1e-6 * ml and abs(st[e, 3] - mt) <= 1e-6 * mt
         assert (st[e, 1], st[e, 2]) == (wtr, wte)
     assert st[-1, 0] < st[0, 0]  # training loss goes down over the epochs
+
+
+def test_session_between_wide_worker_epochs(chaos, torch_cuda):
+    """A session that grows the net's session buffers between two epochs of
+    one-wavefront workers leaves those workers' scratch intact: the second
+    wide epoch at lr 0 claims every sample once and its losses are the
+    oracle's at the session's weights."""
+    torch = torch_cuda
+    net, layers, p = _net(chaos, "small")
+    wmax = net.worker_limit
+    n = 4000
+    x, y = wl.train_set(n)
+    xd, yd = _dev(torch, x, torch.float32), _dev(torch, y, torch.int32)
+    net.train_epoch(xd, yd, 0.0, mode=chaos.HOGWILD_ATOMIC, workers=wmax)
+    xs, ys = wl.train_set(6000)
+    xt, yt = wl.test_set(5000)
+    net.train_session(_dev(torch, xs, torch.float32), _dev(torch, ys, torch.int32),
+                      _dev(torch, xt, torch.float32), _dev(torch, yt, torch.int32), 1, 1e-3, 1.0,
+                      mode=chaos.SEQUENTIAL)
+    w = net.get_params()
+    claims = torch.zeros(n, dtype=torch.int32, device="cuda")
+    net.set_claim_counter(claims)
+    loss = torch.empty(n, device="cuda")
+    net.train_epoch(xd, yd, 0.0, mode=chaos.HOGWILD_ATOMIC, workers=wmax, loss=loss)
+    net.set_claim_counter(None)
+    torch.cuda.synchronize()
+    assert torch.all(claims == 1)
+    assert torch.equal(net.get_params(), w)
+    wc = w.cpu().numpy()
+    ref = np.array([orc.forward_backward(layers, wc, x[i], int(y[i]), grad=False)["loss"]
+                    for i in range(0, n, n // 8)])
+    assert_close(loss.cpu().numpy()[::n // 8], ref, what="losses at lr 0 after the session")
 
 
 @pytest.mark.parametrize("name", ["small", "large", "large_table1"])
