@@ -18,6 +18,9 @@
  *  - One call at a time per chaos_net; different nets are independent.
  *  - Images are fp32, row-major [n][in_h * in_w]; labels int32 in
  *    [0, n_classes) where n_classes is the output size of the last layer.
+ *    Labels live in device memory and are not range-checked: a label
+ *    outside that range only ever enters comparisons (its one-hot target
+ *    is all zeros and an evaluation counts the sample as wrong).
  *  - Canonical parameter layout (get/set, init, gradients): layers in order;
  *    conv: W[o][i][u][v] row-major then b[o]; fully connected: W[j][i] (i over
  *    the map-major flattened input) then b[j]; pooling layers hold nothing.
@@ -34,7 +37,7 @@ extern "C" {
 
 enum {
     CHAOS_OK = 0,
-    CHAOS_EINVAL = -1,      /* null pointer, n < 0, unknown kind/mode, bad label range  */
+    CHAOS_EINVAL = -1,      /* null pointer, n < 0, unknown kind/mode, bad worker count  */
     CHAOS_ESHAPE = -2,      /* kernel > map, pool not dividing the map, n_params mismatch */
     CHAOS_ENOMEM = -3,      /* device or host allocation failed                          */
     CHAOS_EDEVICE = -4,     /* a HIP runtime error; text in chaos_last_error()            */

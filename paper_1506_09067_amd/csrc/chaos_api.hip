@@ -108,6 +108,8 @@ int build_desc(int32_t in_h, int32_t in_w, const chaos_layer *layers, int32_t n_
             ly.wout = (int)(w / src.kernel);
         } else if (src.kind == CHAOS_FC) {
             if (src.maps < 1) return fail(CHAOS_EINVAL, "layer %d: fc neurons=%d", l, src.maps);
+            if (c * h * w > kIntLimit)
+                return fail(CHAOS_EUNSUPPORTED, "layer %d: fc input beyond 2^30", l);
             ly.cin = (int)(c * h * w); ly.hin = 1; ly.win = 1;
             ly.cout = src.maps; ly.hout = 1; ly.wout = 1;
             nw = (int64_t)src.maps * c * h * w;
@@ -115,10 +117,12 @@ int build_desc(int32_t in_h, int32_t in_w, const chaos_layer *layers, int32_t n_
         } else {
             return fail(CHAOS_EINVAL, "layer %d: unknown kind %d", l, src.kind);
         }
-        ly.nin = ly.cin * ly.hin * ly.win;
-        ly.nout = ly.cout * ly.hout * ly.wout;
-        if (nw + nb + off > kIntLimit || (int64_t)ly.nout > kIntLimit)
+        const int64_t nin = (int64_t)ly.cin * ly.hin * ly.win;
+        const int64_t nout = (int64_t)ly.cout * ly.hout * ly.wout;
+        if (nw + nb + off > kIntLimit || nin > kIntLimit || nout > kIntLimit)
             return fail(CHAOS_EUNSUPPORTED, "layer %d: sizes beyond 2^30", l);
+        ly.nin = (int)nin;
+        ly.nout = (int)nout;
         ly.w_off = (int)off;
         ly.b_off = (int)(off + nw);
         ly.nw = (int)nw;

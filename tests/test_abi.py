@@ -58,6 +58,8 @@ def _create(lib, layers, n_params, params=None, in_hw=29):
     ([(3, 0, 0)], 0, -1),                      # FC without neurons
     ([(1, 0, 4)], 0, -1),                      # conv without maps
     ([(1, 5, 4), (2, 0, 2), (3, 10, 0)], 123, -2),  # n_params mismatch
+    ([(1, 1 << 22, 1)], 0, -5),                # 2^22 maps of 29x29: outputs beyond 2^31
+    ([(1, 1 << 20, 1), (3, 4, 0)], 0, -5),     # FC over 2^20 x 841 inputs
 ])
 def test_create_rejects_bad_architectures(lib, layers, n_params, code):
     rc, h = _create(lib, layers, n_params)
