@@ -36,6 +36,7 @@ struct Cpcp {
     static constexpr int CT2 = (C2 + 15) / 16;          // conv2 map tiles
     static constexpr int C2P = CT2 * 16;
     static constexpr int OKS = (C2 + 3) / 4;            // k-steps over output maps
+    static_assert(4 * OKS <= C2P, "every k-step's delta rows lie in the delta buffer");
     // canonical parameter offsets
     static constexpr int OW1 = 0, OB1 = C1 * 16;
     static constexpr int OW2 = OB1 + C1, OB2 = OW2 + C2 * KC2;
@@ -216,7 +217,8 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 for (int s = 0; s < 4; ++s)
 #pragma unroll
                     for (int q = 0; q < 6; ++q) {
-                        float av = valid[q] ? sm.x[base[q] + s * S::IN + lg] : 0.0f;
+                        const float v = sm.x[base[q] + s * S::IN + lg];  // base 0 when invalid
+                        const float av = valid[q] ? v : 0.0f;
 #pragma unroll
                         for (int j = 0; j < S::CT1; ++j) acc[q][j] = mfma(av, bw[s][j], acc[q][j]);
                     }
@@ -300,7 +302,8 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 for (int e = 0; e < 4; ++e) {
 #pragma unroll
                     for (int i = 0; i < 3; ++i) {
-                        float av = pv[i] ? sm.p1[base[i] + offs[e]] : 0.0f;
+                        const float v = sm.p1[base[i] + offs[e]];  // base 0 when invalid
+                        const float av = pv[i] ? v : 0.0f;
 #pragma unroll
                         for (int j = 0; j < S::CT2; ++j) acc[i][j] = mfma(av, b[j][e], acc[i][j]);
                     }
@@ -672,7 +675,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 const int o = 4 * ks + lg;
                 float bv[RT2];
 #pragma unroll
-                for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
+                for (int j = 0; j < RT2; ++j) {
+                    const float v = sm.d2[o * 96 + 16 * j + lr];  // o < C2P: in the buffer
+                    bv[j] = (o < S::C2) ? v : 0.0f;
+                }
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -744,13 +750,19 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                         const int o = 4 * ks + lg;
                         const float *w2 = W2 + (o < S::C2 ? o : 0) * S::W2S;
 #pragma unroll
-                        for (int t = 0; t < TI; ++t) av[t] = (o < S::C2 && wo[t] >= 0) ? w2[wo[t]] : 0.0f;
+                        for (int t = 0; t < TI; ++t) {
+                            const float v = w2[wo[t] >= 0 ? wo[t] : 0];
+                            av[t] = (o < S::C2 && wo[t] >= 0) ? v : 0.0f;
+                        }
                     };
                     auto compute = [&](const float (&av)[TI], int ks) {
                         const int o = 4 * ks + lg;
                         float bv[RT2];
 #pragma unroll
-                        for (int j = 0; j < RT2; ++j) bv[j] = (o < S::C2) ? sm.d2[o * 96 + 16 * j + lr] : 0.0f;
+                        for (int j = 0; j < RT2; ++j) {
+                            const float v = sm.d2[o * 96 + 16 * j + lr];  // o < C2P: in the buffer
+                            bv[j] = (o < S::C2) ? v : 0.0f;
+                        }
 #pragma unroll
                         for (int t = 0; t < TI; ++t)
 #pragma unroll
@@ -829,13 +841,16 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 for (int b = 0; b < JB; ++b)
 #pragma unroll
                     for (int i = 0; i < S::CT2; ++i) acc[b][i] = f4{0.f, 0.f, 0.f, 0.f};
+                // operands: unconditional LDS reads from a clamped address,
+                // zeroed by a select (no branch between a read and its use)
 #pragma unroll
                 for (int s = 0; s < 21; ++s) {
                     float bv[JB];
+                    const int q = pb(s);  // -1 past the map
 #pragma unroll
                     for (int b = 0; b < JB; ++b) {
-                        const int q = pb(s);
-                        bv[b] = (kv[b] && q >= 0) ? pc[b][q] : 0.0f;
+                        const float v = pc[b][q >= 0 ? q : 0];
+                        bv[b] = (kv[b] && q >= 0) ? v : 0.0f;
                     }
 #pragma unroll
                     for (int b = 0; b < JB; ++b)
@@ -891,7 +906,9 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 const float bx = sm.x[2 * py * S::IN + 2 * px + xo];
 #pragma unroll
                 for (int t = 0; t < S::CT1; ++t) {
-                    const float av = (ov[t] && sm.am1[orow[t] + P] == lg) ? sm.e1[orow[t] + P] : 0.0f;
+                    const int am = sm.am1[orow[t] + P];  // orow 0 when the map is past C1
+                    const float v = sm.e1[orow[t] + P];
+                    const float av = (ov[t] && am == lg) ? v : 0.0f;
                     c[t] = mfma(av, bx, c[t]);
                 }
             };
