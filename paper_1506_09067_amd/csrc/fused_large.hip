@@ -883,23 +883,39 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 kval[j] = k < KC2;
                 boff[j] = kval[j] ? sm.koff2[k] : 0;
             }
-            for (int ks = 0; ks < 31; ++ks) {
-                int p = 4 * ks + lg;
-                bool pv = p < NY2;
-                int py = p / H2, px = p - py * H2;
-                int pb = pv ? py * Q1 + px : 0;
-                float av[4], bv[3];
+            // operands: unconditional LDS reads from clamped addresses (a
+            // select zeroes the padding), the next step's read while this
+            // step's matrix instructions run
+            auto load = [&](float (&av)[4], float (&bv)[3], int ks) {
+                const int p = 4 * ks + lg, pc = p < NY2 ? p : 0;
+                const int py = pc / H2, px = pc - py * H2, pb = py * Q1 + px;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    int o = 16 * i + lr;
-                    av[i] = (pv && o < C2) ? sm.y2[o * NY2 + p] : 0.0f;
+                    const int o = 16 * i + lr;
+                    av[i] = sm.y2[(o < C2 ? o : 0) * NY2 + pc];
                 }
 #pragma unroll
-                for (int j = 0; j < 3; ++j) bv[j] = (pv && kval[j]) ? sm.p1[boff[j] + pb] : 0.0f;
+                for (int j = 0; j < 3; ++j) bv[j] = sm.p1[boff[j] + pb];  // boff 0 when invalid
+            };
+            auto step = [&](const float (&av)[4], const float (&bv)[3], int ks) {
+                const bool pv = 4 * ks + lg < NY2;
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
+                for (int i = 0; i < 4; ++i) {
+                    const float a = (pv && 16 * i + lr < C2) ? av[i] : 0.0f;
 #pragma unroll
-                    for (int j = 0; j < 3; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
+                    for (int j = 0; j < 3; ++j) acc[i][j] = mfma(a, kval[j] ? bv[j] : 0.0f, acc[i][j]);
+                }
+            };
+            float aA[4], bA[3], aB[4], bB[3];
+            load(aA, bA, 0);
+            for (int ks = 0; ks < 31; ks += 2) {
+                if (ks + 1 < 31) load(aB, bB, ks + 1);
+                step(aA, bA, ks);
+                if (ks + 1 < 31) {
+                    if (ks + 2 < 31) load(aA, bA, ks + 2);
+                    step(aB, bB, ks + 1);
+                }
             }
 #pragma unroll
             for (int j = 0; j < 3; ++j) {
@@ -941,8 +957,11 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             auto step = [&](int P, f4 (&c)[2]) {
                 const int py = P / Q1, px = P - py * Q1;
                 const float bx = sm.x[2 * py * IN + 2 * px + xo];
-                const float a0 = (sm.am1[oa * NP1 + P] == lg) ? sm.s2[oa * NP1 + P] : 0.0f;
-                const float a1 = (vb && sm.am1[ob * NP1 + P] == lg) ? sm.s2[ob * NP1 + P] : 0.0f;
+                // both reads unconditional (ob is 0 when the map is past C1)
+                const int m0 = sm.am1[oa * NP1 + P], m1 = sm.am1[ob * NP1 + P];
+                const float v0 = sm.s2[oa * NP1 + P], v1 = sm.s2[ob * NP1 + P];
+                const float a0 = (m0 == lg) ? v0 : 0.0f;
+                const float a1 = (vb && m1 == lg) ? v1 : 0.0f;
                 c[0] = mfma(a0, bx, c[0]);
                 c[1] = mfma(a1, bx, c[1]);
             };
