@@ -883,32 +883,38 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
             }
             const int wy = lg >> 1, wx = lg & 1;
             // operands of pooled position P (read one position ahead)
-            auto operands = [&](int P, float (&av)[4], float (&bv)[4]) {
+            // raw reads here, the selects in compute behind a scheduling
+            // barrier: the next position's reads are issued before this
+            // position's matrix instructions wait for anything
+            auto operands = [&](int P, int (&am)[4], float (&av)[4], float (&bv)[4]) {
                 const int py = P / Q2, px = P - py * Q2;
                 const int base = (2 * py + wy) * H1 + 2 * px + wx;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int am = sm.am2[orow[i] + P];
-                    const float v = sm.y2[orow[i] + P];
-                    av[i] = (ovv[i] && am == lg) ? v : 0.0f;
+                    am[i] = sm.am2[orow[i] + P];
+                    av[i] = sm.y2[orow[i] + P];
                 }
 #pragma unroll
                 for (int q = 0; q < 4; ++q) bv[q] = sm.a1[base + ko[q]];
             };
-            auto compute = [&](const float (&av)[4], const float (&bv)[4]) {
+            auto compute = [&](const int (&am)[4], const float (&av)[4], const float (&bv)[4]) {
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
+                for (int i = 0; i < 4; ++i) {
+                    const float a = (ovv[i] && am[i] == lg) ? av[i] : 0.0f;
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) acc[i][q] = mfma(av[i], bv[q], acc[i][q]);
+                    for (int q = 0; q < 4; ++q) acc[i][q] = mfma(a, bv[q], acc[i][q]);
+                }
             };
+            int mA[4], mB[4];
             float aA[4], bA[4], aB[4], bB[4];
-            operands(0, aA, bA);
+            operands(0, mA, aA, bA);
             for (int P = 0; P < NY2; P += 2) {
-                if (P + 1 < NY2) operands(P + 1, aB, bB);
-                compute(aA, bA);
+                if (P + 1 < NY2) operands(P + 1, mB, aB, bB);
+                compute(mA, aA, bA);
                 if (P + 1 < NY2) {
-                    if (P + 2 < NY2) operands(P + 2, aA, bA);
-                    compute(aB, bB);
+                    if (P + 2 < NY2) operands(P + 2, mA, aA, bA);
+                    compute(mB, aB, bB);
                 }
             }
 #pragma unroll
