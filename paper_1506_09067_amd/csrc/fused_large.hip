@@ -310,16 +310,20 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             auto compute = [&](const f4 (&b)[7], int S) {
                 const int4 ko = *(const int4 *)(sm.koff3 + 16 * S + 4 * lg);
                 const int offs[4] = {ko.x, ko.y, ko.z, ko.w};
+                // the super-step's twelve activations are read at once: the
+                // later sub-steps' arrive while the first one computes
+                float av[4][3];
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    float av[3];
+                for (int s = 0; s < 4; ++s)
 #pragma unroll
-                    for (int i = 0; i < 3; ++i) av[i] = sm.y2[base[i] + offs[s]];  // padding rows: unused
+                    for (int i = 0; i < 3; ++i) av[s][i] = sm.y2[base[i] + offs[s]];  // padding rows: unused
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
 #pragma unroll
                     for (int i = 0; i < 3; ++i)
 #pragma unroll
-                        for (int j = 0; j < 7; ++j) acc[i][j] = mfma(av[i], b[j][s], acc[i][j]);
-                }
+                        for (int j = 0; j < 7; ++j) acc[i][j] = mfma(av[s][i], b[j][s], acc[i][j]);
             };
             // weights two super-steps ahead (a ring of three buffers)
             load_b(bA, S0);
@@ -722,18 +726,23 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 }
                 const int k4 = 64 * grp + lane;
                 const float *y4 = sm.y2 + (k4 < KC3 ? sm.koff3[k4] : 0);
+                // the group's 36 activations are read at once: later steps'
+                // arrive while the first ones compute
+                float bv[18][2];
 #pragma unroll
                 for (int ms = 0; ms < 18; ++ms) {
                     const int m = 2 * ms + (lane >> 5), wp = window_pos(m >> 2, m & 3, 3, H2);
-                    float bv[2];
 #pragma unroll
-                    for (int kt = 0; kt < 2; ++kt) bv[kt] = y32[kt][wp];
+                    for (int kt = 0; kt < 2; ++kt) bv[ms][kt] = y32[kt][wp];
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int ms = 0; ms < 18; ++ms)
 #pragma unroll
                     for (int i = 0; i < 3; ++i)
 #pragma unroll
                         for (int kt = 0; kt < 2; ++kt)
-                            c32[i][kt] = mfma32(a32[i][ms], bv[kt], ms == 0 ? f16{} : c32[i][kt]);
-                }
+                            c32[i][kt] = mfma32(a32[i][ms], bv[ms][kt], ms == 0 ? f16{} : c32[i][kt]);
                 // two partial sums (even and odd m) keep the chain short
 #pragma unroll
                 for (int m = 0; m < M3; ++m) {
