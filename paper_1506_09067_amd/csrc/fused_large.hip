@@ -297,7 +297,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 base[i] = valid[i] ? window_pos(m >> 2, m & 3, 3, H2) : 0;
             }
             const int S0 = wave * 34, S1 = (S0 + 34 < 135) ? S0 + 34 : 135;
-            f4 bA[7], bB[7], bC[7];
+            f4 bA[7], bB[7], bC[7], bD[7];
             auto load_b = [&](f4 (&b)[7], int S) {
 #pragma unroll
                 for (int j = 0; j < 7; ++j) {
@@ -325,19 +325,24 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
 #pragma unroll
                         for (int j = 0; j < 7; ++j) acc[i][j] = mfma(av[s][i], b[j][s], acc[i][j]);
             };
-            // weights two super-steps ahead (a ring of three buffers)
+            // weights three super-steps ahead (a ring of four buffers)
             load_b(bA, S0);
             if (S0 + 1 < S1) load_b(bB, S0 + 1);
-            for (int S = S0; S < S1; S += 3) {
-                if (S + 2 < S1) load_b(bC, S + 2);
+            if (S0 + 2 < S1) load_b(bC, S0 + 2);
+            for (int S = S0; S < S1; S += 4) {
+                if (S + 3 < S1) load_b(bD, S + 3);
                 compute(bA, S);
                 if (S + 1 < S1) {
-                    if (S + 3 < S1) load_b(bA, S + 3);
+                    if (S + 4 < S1) load_b(bA, S + 4);
                     compute(bB, S + 1);
                 }
                 if (S + 2 < S1) {
-                    if (S + 4 < S1) load_b(bB, S + 4);
+                    if (S + 5 < S1) load_b(bB, S + 5);
                     compute(bC, S + 2);
+                }
+                if (S + 3 < S1) {
+                    if (S + 6 < S1) load_b(bC, S + 6);
+                    compute(bD, S + 3);
                 }
             }
             // fixed-order reduction (w0 + w2) + (w1 + w3) through LDS; the
@@ -652,7 +657,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 for (int j = 0; j < 3; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
             const int k0 = blk * 144;
             const int arow = k0 + (lr >> 2) * 36 + (lr & 3);
-            float aA[9], aB[9], bA[3], bB[3];
+            float aA[9], aB[9], aC[9], aD[9], bA[3], bB[3], bC[3], bD[3];
             auto load = [&](float (&av)[9], float (&bv)[3], int ks) {
                 const float *w3 = W + DW3 + (4 * ks + lg) * KC3 + arow;
 #pragma unroll
@@ -662,20 +667,34 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 for (int j = 0; j < 3; ++j) bv[j] = dd[16 * j];
             };
             auto compute = [&](const float (&av)[9], const float (&bv)[3]) {
+                // keeps the weight reads of the steps ahead issued before
+                // these matrix instructions wait for this step's
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int i = 0; i < 9; ++i)
 #pragma unroll
                     for (int j = 0; j < 3; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
             };
-            // the next output maps' weights and deltas are loaded while the
-            // current ones compute
+            // weights and deltas three output-map steps ahead (a ring of four
+            // buffers): under the update stream a weight read waits microseconds
+            constexpr int NKS = C3 / 4;
             load(aA, bA, 0);
-            for (int ks = 0; ks < C3 / 4; ks += 2) {
-                if (ks + 1 < C3 / 4) load(aB, bB, ks + 1);
+            load(aB, bB, 1);
+            load(aC, bC, 2);
+            for (int ks = 0; ks < NKS; ks += 4) {
+                if (ks + 3 < NKS) load(aD, bD, ks + 3);
                 compute(aA, bA);
-                if (ks + 1 < C3 / 4) {
-                    if (ks + 2 < C3 / 4) load(aA, bA, ks + 2);
+                if (ks + 1 < NKS) {
+                    if (ks + 4 < NKS) load(aA, bA, ks + 4);
                     compute(aB, bB);
+                }
+                if (ks + 2 < NKS) {
+                    if (ks + 5 < NKS) load(aB, bB, ks + 5);
+                    compute(aC, bC);
+                }
+                if (ks + 3 < NKS) {
+                    if (ks + 6 < NKS) load(aC, bC, ks + 6);
+                    compute(aD, bD);
                 }
             }
             float *dst = sm.s2 + (4 * blk + lg) * NY2;
