@@ -38,7 +38,7 @@ def _train_and_test(torch, chaos, name, x, y, xt, yt, epochs, lr, decay, mode, w
     w = net.get_params()
     torch.cuda.synchronize()
     assert torch.isfinite(w).all()
-    return float(loss.double().mean()), 1.0 - int(wrong.item()) / len(yt), net.max_workers
+    return float(loss.double().mean()), int(wrong.item()), net.max_workers
 
 
 # (net, training samples, epochs, lr, Hogwild workers; 0 = every resident worker).
@@ -53,7 +53,7 @@ CASES = [
     ("medium", 60000, 3, 1e-3, 0),
     ("large", 60000, 1, 1e-3, 0),
     ("large", 60000, 1, 1e-3, 64),
-    ("large_table1", 20000, 1, 1e-3, 0),
+    ("large_table1", 30000, 1, 1e-3, 0),
 ]
 
 
@@ -70,8 +70,10 @@ def test_hogwild_matches_sequential_sgd(env, name, n, epochs, lr, workers):
     init = _train_and_test(torch, chaos, name, x[:0], y[:0], xt, yt, 1, lr, decay,
                            chaos.SEQUENTIAL, 0)
     assert seq[0] < init[0]
-    msg = (f"{name}: sequential loss {seq[0]:.5f} acc {seq[1]:.4f}; Hogwild with "
-           f"{workers or hog[2]} workers loss {hog[0]:.5f} acc {hog[1]:.4f}; "
+    nt = len(yt)
+    msg = (f"{name}: sequential loss {seq[0]:.5f} wrong {seq[1]}/{nt}; Hogwild with "
+           f"{workers or hog[2]} workers loss {hog[0]:.5f} wrong {hog[1]}/{nt}; "
            f"untrained loss {init[0]:.5f}")
     assert abs(hog[0] - seq[0]) <= 0.01 * seq[0], msg
-    assert abs(hog[1] - seq[1]) <= 0.01, msg
+    # accuracy within one percentage point, counted in whole test images
+    assert 100 * abs(hog[1] - seq[1]) <= nt, msg
