@@ -334,6 +334,61 @@ def training_session(chaos, wl, torch, name, epochs, lr, decay, seq_epochs):
     return out
 
 
+def delay_sweep(chaos, wl, torch, epochs=5, lr=1e-3, decay=0.9):
+    """Delayed pushes on the small net (chaos_set_push_delay): training
+    samples/s at every resident worker for push delays k = 1 (the per-layer
+    push), 2, 4, ..., 64 (two timed 60,000-sample epochs each, after one
+    warm-up epoch), and the test-set loss and wrong count after `epochs`
+    epochs (lr decaying by `decay` per epoch) against sequential per-sample
+    SGD on the same data, with the push of a k-sample sum at lr and at lr / k
+    (the mean of the k gradients)."""
+    layers = wl.NETS["small"]
+    p0 = wl.init_params(layers)
+    x, y = wl.train_set(60000)
+    xt, yt = wl.test_set(10000)
+    xd, yd = torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda()
+    xtd, ytd = torch.from_numpy(xt).cuda(), torch.from_numpy(yt).cuda()
+    flops, _ = train_flops_per_sample(layers)
+
+    def quality(net, mode, lr=lr):
+        for e in range(epochs):
+            net.train_epoch(xd, yd, lr * decay ** e, mode=mode)
+        loss = torch.empty(10000, device="cuda")
+        net.forward_backward(xtd, ytd, loss=loss)
+        wrong = net.evaluate(xtd, ytd)
+        torch.cuda.synchronize()
+        return float(loss.double().mean()), int(wrong.item())
+
+    seq = quality(chaos.Net(layers, p0), chaos.SEQUENTIAL)
+    points = []
+    for k in (1, 2, 4, 8, 16, 32, 64):
+        net = chaos.Net(layers, p0)
+        net.set_push_delay(k)
+        net.train_epoch(xd, yd, lr)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(2):
+            net.train_epoch(xd, yd, lr)
+        b.record()
+        torch.cuda.synchronize()
+        sps = 2 * 60000 / (a.elapsed_time(b) / 1e3)
+        q = quality(_fresh(chaos, layers, p0, k), chaos.HOGWILD_ATOMIC)
+        qm = quality(_fresh(chaos, layers, p0, k), chaos.HOGWILD_ATOMIC, lr / k)
+        points.append({"push_delay": k, "workers": net.max_workers, "samples_per_s": sps,
+                       "tflops": sps * flops / 1e12, "test_loss": q[0], "test_wrong": q[1],
+                       "test_loss_lr_over_k": qm[0], "test_wrong_lr_over_k": qm[1]})
+    return {"sweep": "small net, delayed pushes (atomic Hogwild, every resident worker)",
+            "epochs_for_quality": epochs, "lr": lr, "decay": decay,
+            "sequential": {"test_loss": seq[0], "test_wrong": seq[1]}, "points": points}
+
+
+def _fresh(chaos, layers, p0, k):
+    net = chaos.Net(layers, p0)
+    net.set_push_delay(k)
+    return net
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -358,6 +413,10 @@ def main():
                          "Testing session of EPOCHS epochs of --net with every resident worker "
                          "(and --seq-epochs epochs with one worker) and print per-epoch "
                          "statistics as one JSON line")
+    ap.add_argument("--delay-sweep", action="store_true",
+                    help="instead of the benchmark line, print one JSON line with the small "
+                         "net's training throughput and final test loss against the push "
+                         "delay (chaos_set_push_delay)")
     ap.add_argument("--seq-epochs", type=int, default=1)
     ap.add_argument("--decay", type=float, default=1.0)
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -388,6 +447,9 @@ def main():
         return
     if args.model:
         print(json.dumps(model_fit(chaos, wl, torch, args.net)), flush=True)
+        return
+    if args.delay_sweep:
+        print(json.dumps(delay_sweep(chaos, wl, torch)), flush=True)
         return
     if args.session:
         print(json.dumps(training_session(chaos, wl, torch, args.net, args.session, 1e-3,

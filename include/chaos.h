@@ -171,6 +171,20 @@ int32_t chaos_max_workers(const chaos_net *net);
  * up to 32 per compute unit (>= chaos_max_workers). */
 int32_t chaos_worker_limit(const chaos_net *net);
 
+/* Delayed pushes (a variant of the per-layer update, Section III-A.2, with
+ * delayed sharing of locally accumulated updates): with k > 1, every worker
+ * of a CHAOS_HOGWILD_ATOMIC epoch adds its per-layer gradients to a private
+ * sum and pushes W <- W - lr * sum after every k-th sample it processes and
+ * after its last; a worker does not see its own unpushed updates, so one
+ * worker is mini-batch SGD with batches of k consecutive samples.  k = 1
+ * (the default) is the per-layer push.  CHAOS_SEQUENTIAL and
+ * CHAOS_HOGWILD_RACY epochs ignore the setting.  Only the small net of
+ * Table I supports k > 1 (its weights and the sum fit in LDS), else
+ * CHAOS_EUNSUPPORTED; k < 1 is CHAOS_EINVAL.  While k > 1,
+ * chaos_max_workers() reports the delayed kernel's capacity and larger
+ * worker counts are CHAOS_EINVAL. */
+int chaos_set_push_delay(chaos_net *net, int32_t k);
+
 /* Debug aid: when claims_dev (int32 [n] of the next chaos_train_epoch) is not
  * NULL, every processed sample index i adds 1 to claims_dev[i]; NULL turns it
  * off.  The buffer must hold at least n entries for each later call. */

@@ -63,6 +63,7 @@ def lib():
             "chaos_max_workers": ([P], ctypes.c_int32),
             "chaos_worker_limit": ([P], ctypes.c_int32),
             "chaos_set_claim_counter": ([P, P], ctypes.c_int),
+            "chaos_set_push_delay": ([P, i32], ctypes.c_int),
             "chaos_last_error": ([], ctypes.c_char_p),
         }
         for name, (args, res) in sig.items():
@@ -209,3 +210,7 @@ class Net:
     def set_claim_counter(self, claims):
         _check(lib().chaos_set_claim_counter(
             self._h, _dev(claims, torch.int32, "claims", optional=True)))
+
+    def set_push_delay(self, k: int):
+        """Samples between a worker's pushes in atomic Hogwild epochs (1 = per layer)."""
+        _check(lib().chaos_set_push_delay(self._h, int(k)))

@@ -38,6 +38,8 @@ struct chaos_net {
     float *sess_loss = nullptr;   // session: per-sample losses (training, then test)
     int64_t sess_loss_n = 0;
     int32_t *sess_wrong = nullptr;
+    int push_delay = 1;           // samples between a worker's pushes (atomic Hogwild)
+    int delay_max_workers = 0;    // resident workers of the delayed-push kernel (0 = none)
 };
 
 namespace {
@@ -184,6 +186,7 @@ chaos::WorkArgs base_args(chaos_net *net, const float *x, const int32_t *labels,
     a.n = n;
     a.scratch = net->scratch;
     a.counter = net->counter;
+    a.push_delay = 1;
     return a;
 }
 
@@ -230,6 +233,7 @@ int chaos_create_net(int32_t in_h, int32_t in_w, const chaos_layer *layers, int3
                             : chaos::worker_blocks_per_cu(net->block);
     if (per_cu < 1) { delete net; return fail(CHAOS_EDEVICE, "occupancy query failed"); }
     net->max_workers = per_cu * cus;
+    net->delay_max_workers = net->cpcp ? chaos::fused_cpcp_delay_blocks_per_cu(net->cpcp) * cus : 0;
     net->worker_limit = std::max(net->max_workers, chaos::worker_blocks_per_cu(64) * cus);
     // the fused kernels keep every per-sample value in LDS: no scratch
     size_t scratch_bytes = (net->fused || net->t1 || net->cpcp)
@@ -303,7 +307,16 @@ int32_t chaos_num_outputs(const chaos_net *net) {
 
 int32_t chaos_max_workers(const chaos_net *net) {
     if (int rc = check_net(net)) return rc;
-    return net->max_workers;
+    return net->push_delay > 1 ? net->delay_max_workers : net->max_workers;
+}
+
+int chaos_set_push_delay(chaos_net *net, int32_t k) {
+    if (int rc = check_net(net)) return rc;
+    if (k < 1) return fail(CHAOS_EINVAL, "push delay %d < 1", k);
+    if (k > 1 && net->delay_max_workers < 1)
+        return fail(CHAOS_EUNSUPPORTED, "delayed pushes need a net whose weights fit in LDS");
+    net->push_delay = k;
+    return ok();
 }
 
 int32_t chaos_worker_limit(const chaos_net *net) {
@@ -370,6 +383,21 @@ int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_
         return fail(CHAOS_EINVAL, "workers=%d outside [0,%d]", workers, net->worker_limit);
     if (int rc = set_device(net)) return rc;
     if (n == 0) return ok();
+    if (mode == CHAOS_HOGWILD_ATOMIC && net->push_delay > 1) {
+        // delayed pushes: the net's own kernel with a per-worker gradient sum
+        if (workers > net->delay_max_workers)
+            return fail(CHAOS_EINVAL, "workers=%d: delayed pushes run at most %d workers", workers,
+                        net->delay_max_workers);
+        chaos::WorkArgs a = base_args(net, x_dev, labels_dev, n);
+        a.lr = lr;
+        a.loss = loss_dev;
+        a.claims = net->claims;
+        a.push_delay = net->push_delay;
+        int grid = (int)std::min<int64_t>(workers == 0 ? net->delay_max_workers : workers, n);
+        HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 2, stream), "counter reset");
+        HIP_TRY(launch(net, chaos::kTrainAtomic, a, grid, stream), "train launch");
+        return ok();
+    }
     if (mode != CHAOS_SEQUENTIAL && workers > net->max_workers) {
         // more workers than the net's kernel keeps resident: every worker is one
         // 64-thread wavefront of the generic kernel, with scratch in HBM

@@ -51,6 +51,7 @@ struct WorkArgs {
     float *grad_part;      // [workers][n_params] optional (frozen-weight sums)
     int32_t *n_wrong;      // [1] evaluation
     int32_t *claims;       // [n] optional debug claim counter
+    int32_t push_delay;    // training: samples between a worker's pushes (1 = per layer)
 };
 
 // Device layout of a net's shared weights, as segments of the canonical
@@ -107,5 +108,7 @@ int fused_cpcp_variant(const Net &net);  // 0 when the net is neither
 bool fused_cpcp_layout(int variant, ParamLayout &L);
 hipError_t launch_fused_cpcp(int variant, int mode, const WorkArgs &a, int grid, hipStream_t s);
 int fused_cpcp_blocks_per_cu(int variant);
+// resident workers per CU of the small net's delayed-push kernel (0 for others)
+int fused_cpcp_delay_blocks_per_cu(int variant);
 
 } // namespace chaos

@@ -76,7 +76,7 @@ struct Cpcp {
 constexpr int NT = 256, NW = 4;
 constexpr int RT2 = 6;  // conv2 output positions 81 -> 6 tiles of 16
 
-template <class S>
+template <class S, bool DELAY = false>
 struct alignas(16) SmemCpcp {
     float x[S::NX + 3];
     float p1[S::C1 * S::NP1];            // pool1 output, later pool1 errors/deltas in e1
@@ -94,12 +94,23 @@ struct alignas(16) SmemCpcp {
     alignas(16) float w[S::STAGE ? S::NPARAM4 : 4];  // the weights read at the start of the sample
     alignas(16) float w2[S::STAGE2 ? S::NW2 : 4];    // the conv2 weights read at the start of the sample
     float sink[64];                      // scatter target of padding lanes
+    // delayed pushes: this worker's gradient sum since its last push
+    alignas(16) float gacc[DELAY ? S::NPARAM4 : 4];
     int64_t idx;
 };
 
-template <class S, int MODE, int MINB>
+// DELAY (training with atomic pushes, nets whose whole weight vector fits in
+// LDS): instead of pushing each layer's gradient after its backward pass,
+// the worker adds it to a private sum in LDS and pushes the sum after every
+// a.push_delay samples it processes, and after its last (a variant of the
+// per-layer update, Section III-A.2, with the delayed sharing of locally
+// accumulated updates); its own unpushed updates are not in the weights it
+// reads.
+template <class S, int MODE, int MINB, bool DELAY = false>
 __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
-    __shared__ SmemCpcp<S> sm;
+    static_assert(!DELAY || (MODE == kTrainAtomic && S::STAGE && !S::PAD),
+                  "delayed pushes: atomic training of a net copied whole into LDS, canonical layout");
+    __shared__ SmemCpcp<S, DELAY> sm;
     const float *Wg = a.params;
     // every weight read below goes through W: the LDS copy or the shared vector
     const float *W = S::STAGE ? (const float *)sm.w : Wg;
@@ -114,6 +125,26 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         int c = k / 25, uv = k - 25 * c, u = uv / 5, v = uv - 5 * u;
         sm.koff2[k] = (k < S::KC2) ? c * S::NP1 + u * S::Q1 + v : 0;
     }
+    int nproc = 0;  // samples this worker has processed (delayed pushes)
+    if constexpr (DELAY) {
+        for (int i = threadIdx.x; i < S::NPARAM; i += NT) sm.gacc[i] = 0.0f;
+    }
+    // pushes this worker's gradient sum (W += -lr * sum, the rounding of the
+    // per-layer push) and clears it; after a barrier
+    auto flush = [&]() {
+        if constexpr (DELAY) {
+            Push fp;
+            fp.mode = kTrainAtomic;
+            fp.params = a.params;
+            fp.neg_lr = -a.lr;
+            fp.each = nullptr;
+            fp.part = nullptr;
+            for (int i = threadIdx.x; i < S::NPARAM; i += NT) {
+                fp(i, sm.gacc[i]);
+                sm.gacc[i] = 0.0f;
+            }
+        }
+    };
 
     // Training: thread 0 claims the worker's next sample as soon as the
     // current one is known (Section III-A.1), so the claim's round trip to
@@ -142,7 +173,12 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         if (kTrain && wave == 0) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         __syncthreads();
         const int64_t idx = sm.idx;
-        if (idx >= a.n) break;
+        if (idx >= a.n) {
+            if constexpr (DELAY) {
+                if (nproc % a.push_delay) flush();
+            }
+            break;
+        }
         if (kTrain && tid == 0) {
             next = atomicAdd(a.counter, 1);
             if (a.claims) atomicAdd(a.claims + idx, 1);
@@ -463,12 +499,18 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         }
 
         // ================= back-propagation =================
-        Push push;
-        push.mode = MODE;
-        push.params = a.params;
-        push.neg_lr = -a.lr;
-        push.each = a.grad_each ? a.grad_each + idx * (int64_t)S::NPARAM : nullptr;
-        push.part = a.grad_part ? a.grad_part + (int64_t)blockIdx.x * S::NPARAM : nullptr;
+        Push push_now;
+        push_now.mode = MODE;
+        push_now.params = a.params;
+        push_now.neg_lr = -a.lr;
+        push_now.each = a.grad_each ? a.grad_each + idx * (int64_t)S::NPARAM : nullptr;
+        push_now.part = a.grad_part ? a.grad_part + (int64_t)blockIdx.x * S::NPARAM : nullptr;
+        // a layer's gradient element (each weight once per sample, by one
+        // thread): pushed now, or added to the worker's sum
+        auto push = [&](int w_off, int g_off, float g) {
+            if constexpr (DELAY) sm.gacc[g_off] += g;
+            else push_now(w_off, g_off, g);
+        };
 
         if (tid < 64) {
             float e = 0.0f;
@@ -605,7 +647,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                         for (int c = 0; c < IC; ++c) {
                             int i = lane + 64 * c;
-                            old[r][c] = (i < S::NF1) ? push.with_old(S::DF1 + jr * S::NF1S + i, S::OF1 + jr * S::NF1 + i, dr[r] * xv[c])
+                            old[r][c] = (i < S::NF1) ? push_now.with_old(S::DF1 + jr * S::NF1S + i, S::OF1 + jr * S::NF1 + i, dr[r] * xv[c])
                                                      : 0.0f;
                         }
                     } else {
@@ -940,6 +982,12 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 }
             }
         }
+        if constexpr (DELAY) {
+            if (++nproc % a.push_delay == 0) {
+                __syncthreads();
+                flush();
+            }
+        }
         if (kTrain && tid == 0) atomicAdd(a.counter + 1, 1);  // samples completed
         __syncthreads();
     }
@@ -975,8 +1023,10 @@ int cpcp_blocks_per_cu() {
 }
 
 constexpr int kSmallMinBlocks = 3, kMediumMinBlocks = Medium::STAGE2 ? 1 : 2;
+constexpr int kSmallDelayMinBlocks = 2;  // the gradient sum takes another 25.6 KB
 static_assert(sizeof(SmemCpcp<Small>) * kSmallMinBlocks <= 160 * 1024 &&
-                  sizeof(SmemCpcp<Medium>) * kMediumMinBlocks <= 160 * 1024,
+                  sizeof(SmemCpcp<Medium>) * kMediumMinBlocks <= 160 * 1024 &&
+                  sizeof(SmemCpcp<Small, true>) * kSmallDelayMinBlocks <= 160 * 1024,
               "resident workers per CU fit in the LDS");
 
 bool matches(const Net &net, int c1, int c2, int f1) {
@@ -1026,6 +1076,10 @@ bool fused_cpcp_layout(int variant, ParamLayout &L) {
 }
 
 hipError_t launch_fused_cpcp(int variant, int mode, const WorkArgs &a, int grid, hipStream_t s) {
+    if (variant == 1 && mode == kTrainAtomic && a.push_delay > 1) {
+        fused_cpcp_kernel<Small, kTrainAtomic, kSmallDelayMinBlocks, true><<<grid, NT, 0, s>>>(a);
+        return hipGetLastError();
+    }
     if (variant == 1) return launch_cpcp<Small, kSmallMinBlocks>(mode, a, grid, s);
     if (variant == 2) return launch_cpcp<Medium, kMediumMinBlocks>(mode, a, grid, s);
     return hipErrorInvalidValue;
@@ -1035,6 +1089,16 @@ int fused_cpcp_blocks_per_cu(int variant) {
     if (variant == 1) return cpcp_blocks_per_cu<Small, kSmallMinBlocks>();
     if (variant == 2) return cpcp_blocks_per_cu<Medium, kMediumMinBlocks>();
     return 0;
+}
+
+int fused_cpcp_delay_blocks_per_cu(int variant) {
+    if (variant != 1) return 0;
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &nb, fused_cpcp_kernel<Small, kTrainAtomic, kSmallDelayMinBlocks, true>, NT, 0) !=
+        hipSuccess)
+        return 0;
+    return nb;
 }
 
 } // namespace chaos

@@ -86,4 +86,5 @@ def test_null_and_range_arguments(lib):
     assert lib.chaos_apply_update(None, None, 0.0, None) == -1
     assert lib.chaos_train_session(None, None, None, 0, None, None, 0, 1, 0.0, 1.0, 0, 0, None,
                                    None, None) == -1
+    assert lib.chaos_set_push_delay(None, 2) == -1
     assert lib.chaos_destroy_net(None) == 0
