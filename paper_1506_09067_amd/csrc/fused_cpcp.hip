@@ -9,7 +9,9 @@
 // implicit GEMMs on v_mfma_f32_16x16x4_f32; the 3x3 pool and the fully
 // connected layers run on the vector ALUs.  Per layer the partial derivatives
 // of the layer below are computed from the layer's weights before the layer's
-// gradient is pushed (Section III-A.2), lock-free (III-A.3).
+// gradient is pushed (Section III-A.2), lock-free (III-A.3).  A separate
+// instantiation for the small net keeps each worker's gradient sum in LDS and
+// pushes it every few samples instead (delayed pushes).
 #include "chaos_internal.h"
 #include "device_common.h"
 
