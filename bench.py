@@ -510,8 +510,12 @@ def main():
         net.forward_backward(xbd, ybd, grad_sum=g)
         b.record(stream)
         torch.cuda.synchronize()
-        rows["batch_gradient_16384"] = {"samples_per_s": 16384 / (a.elapsed_time(b) / 1e3),
-                                        "ms": a.elapsed_time(b)}
+        bg_sps = 16384 / (a.elapsed_time(b) / 1e3)
+        bg_flops = flops - 2 * net.n_params  # forward + backward, no update
+        rows["batch_gradient_16384"] = {"samples_per_s": bg_sps, "ms": a.elapsed_time(b),
+                                        "flop_per_sample": bg_flops,
+                                        "tflops": bg_sps * bg_flops / 1e12,
+                                        "frac_fp32_peak": bg_sps * bg_flops / 1e12 / PEAK_FP32_TFLOPS}
         if not args.no_cpu_baseline:
             rows["batch_gradient_16384"]["cpu_oracle"] = cpu_batch_baseline(layers, p0, xb, yb)
         xt, yt = wl.test_set(10000)
@@ -525,6 +529,8 @@ def main():
         rows["test_forward_10000"] = {"samples_per_s": 10000 / (a.elapsed_time(b) / 1e3),
                                       "ms": a.elapsed_time(b),
                                       "tflops": fwd_flops * 10000 / (a.elapsed_time(b) / 1e3) / 1e12,
+                                      "frac_fp32_peak": fwd_flops * 10000 / (a.elapsed_time(b) / 1e3)
+                                      / 1e12 / PEAK_FP32_TFLOPS,
                                       "n_wrong": int(wrong.item())}
 
     upd = update_stream(torch, net.n_params, value) if mode != chaos.SEQUENTIAL else None
