@@ -8,7 +8,8 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libchaos.so")
-SOURCES = ["worker.hip", "fused_large.hip", "fused_t1.hip", "fused_cpcp.hip", "chaos_api.hip"]
+SOURCES = ["worker.hip", "fused_large.hip", "fused_t1.hip", "fused_cpcp.hip", "batch_grad.hip",
+           "chaos_api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

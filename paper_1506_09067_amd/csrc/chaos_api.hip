@@ -38,6 +38,10 @@ struct chaos_net {
     float *sess_loss = nullptr;   // session: per-sample losses (training, then test)
     int64_t sess_loss_n = 0;
     int32_t *sess_wrong = nullptr;
+    float *stash = nullptr;       // large net, batch gradient: per-sample conv3 / FC1 operands
+    int64_t stash_n = 0;          // samples the stash holds
+    float *bpart = nullptr;       // their chunk partial sums: conv3 rows, then FC1 rows
+    int64_t bpart_chunks = 0;
     int push_delay = 1;           // samples between a worker's pushes (atomic Hogwild)
     int delay_max_workers = 0;    // resident workers of the delayed-push kernel (0 = none)
 };
@@ -291,6 +295,8 @@ int chaos_destroy_net(chaos_net *net) {
     (void)hipFree(net->wide_scratch);
     (void)hipFree(net->sess_loss);
     (void)hipFree(net->sess_wrong);
+    (void)hipFree(net->stash);
+    (void)hipFree(net->bpart);
     delete net;
     return ok();
 }
@@ -479,11 +485,40 @@ int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *la
         }
         grid = want;
     }
+    // large net, gradient sum only: the conv3 and FC1 weight gradients are
+    // contracted over the batch on the matrix cores from per-sample operands
+    // the kernel leaves in HBM (47.6 KB per sample, allocated on first use)
+    const bool batched = grad_sum_dev && !grad_each_dev && net->fused;
+    constexpr int64_t kConv3W = 100 * 2160, kFc1W = 150 * 900;
+    if (batched) {
+        if (n > net->stash_n) {
+            (void)hipFree(net->stash);
+            net->stash = nullptr;
+            net->stash_n = 0;
+            if (hipMalloc(&net->stash, (size_t)n * chaos::kStashFloats * sizeof(float)) != hipSuccess) {
+                net->stash = nullptr;
+                return fail(CHAOS_ENOMEM, "batch gradient operands for %lld samples", (long long)n);
+            }
+            net->stash_n = n;
+        }
+        const int64_t nc = chaos::batch_grad_chunks(n);
+        if (nc > net->bpart_chunks) {
+            (void)hipFree(net->bpart);
+            net->bpart = nullptr;
+            net->bpart_chunks = 0;
+            if (hipMalloc(&net->bpart, (size_t)nc * (kConv3W + kFc1W) * sizeof(float)) != hipSuccess) {
+                net->bpart = nullptr;
+                return fail(CHAOS_ENOMEM, "batch gradient partial sums");
+            }
+            net->bpart_chunks = nc;
+        }
+    }
     chaos::WorkArgs a = base_args(net, x_dev, labels_dev, n);
     a.out = out_dev;
     a.loss = loss_dev;
     a.grad_each = grad_each_dev;
     a.grad_part = grad_sum_dev ? net->grad_part : nullptr;
+    a.stash = batched ? net->stash : nullptr;
     if (grad_sum_dev)
         HIP_TRY(chaos::launch_fill_f32(net->grad_part, 0.0f, (int64_t)grid * net->n_params, stream),
                 "zero partial sums");
@@ -492,6 +527,19 @@ int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *la
         HIP_TRY(chaos::launch_reduce_partials(net->grad_part, grid, net->n_params, grad_sum_dev,
                                               stream),
                 "reduce");
+    if (batched) {
+        // the per-sample pass pushed nothing into these two weight blocks:
+        // their sums replace the zeros the reduction left there
+        const int64_t nc = chaos::batch_grad_chunks(n);
+        float *part3 = net->bpart, *partf = net->bpart + nc * kConv3W;
+        HIP_TRY(chaos::launch_batch_grad(net->stash, n, part3, partf, stream), "batch gradient");
+        HIP_TRY(chaos::launch_reduce_partials(part3, nc, kConv3W, grad_sum_dev + net->desc.L[3].w_off,
+                                              stream),
+                "reduce conv3");
+        HIP_TRY(chaos::launch_reduce_partials(partf, nc, kFc1W, grad_sum_dev + net->desc.L[5].w_off,
+                                              stream),
+                "reduce FC1");
+    }
     return ok();
 }
 

@@ -52,6 +52,8 @@ struct WorkArgs {
     int32_t *n_wrong;      // [1] evaluation
     int32_t *claims;       // [n] optional debug claim counter
     int32_t push_delay;    // training: samples between a worker's pushes (1 = per layer)
+    float *stash;          // frozen weights, large net: per-sample operands of the
+                           // batched conv3 / FC1 weight gradients, or null
 };
 
 // Device layout of a net's shared weights, as segments of the canonical
@@ -100,6 +102,17 @@ bool fused_t1_matches(const Net &net);
 void fused_t1_layout(ParamLayout &L);  // its padded device layout
 hipError_t launch_fused_t1(int mode, const WorkArgs &a, int grid, hipStream_t s);
 int fused_t1_blocks_per_cu();
+
+// Batched conv3 and FC1 weight gradients of the large net over a frozen-
+// weight batch (batch_grad.hip).  stash holds, for n samples, d3 [n][100][36],
+// y2 [n][60][121], dh [n][150] and p3 [n][900] one after the other; part3
+// receives batch_grad_chunks(n) partial rows of 100 x 2160 floats, partf as
+// many of 150 x 900, one per chunk of samples (at least kBatchChunk).
+constexpr int kBatchChunk = 64;
+constexpr int64_t kStashFloats = 100 * 36 + 60 * 121 + 150 + 900;  // per sample
+int64_t batch_grad_chunks(int64_t n);
+hipError_t launch_batch_grad(const float *stash, int64_t n, float *part3, float *partf,
+                             hipStream_t s);
 
 // Fused MFMA workers for the Table I small (variant 1) and medium (variant 2)
 // nets: conv C1@4x4, max2, conv C2@5x5, max3, FC F1, FC10 on 29x29 inputs.

@@ -562,7 +562,15 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 }
                 *(f4 *)(sm.e3 + 4 * tid) = acc;
             }
-            {
+            if (a.stash) {
+                // batched gradient: this sample's FC1 deltas and inputs go to
+                // HBM; the FC1 weight gradient is contracted over the batch
+                // afterwards
+                float *dhs = a.stash + a.n * (int64_t)(C3 * M3 + C2 * NY2) + idx * F1;
+                float *p3s = a.stash + a.n * (int64_t)(C3 * M3 + C2 * NY2 + F1) + idx * NF1;
+                if (tid < F1) dhs[tid] = sm.dh[tid];
+                for (int i = tid; i < NF1; i += NT) p3s[i] = sm.p3[i];
+            } else {
                 float xv[15];
 #pragma unroll
                 for (int c = 0; c < 15; ++c) {
@@ -718,6 +726,25 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         }
         __syncthreads();
 
+        // batched gradient (frozen weights, a.stash): this sample's conv3
+        // output deltas and conv3 inputs go to HBM, and the conv3 weight
+        // gradient is contracted over the batch afterwards; the bias
+        // gradient is pushed as usual
+        if (MODE == kForwardBackward && a.stash) {
+            float *d3s = a.stash + idx * (C3 * M3);
+            float *y2s = a.stash + a.n * (int64_t)(C3 * M3) + idx * (C2 * NY2);
+            for (int t = tid; t < C3 * M3; t += NT) {
+                const int o = t / M3, m = t - o * M3;
+                d3s[t] = sm.d3[o * M3P + m];
+            }
+            for (int t = tid; t < C2 * NY2; t += NT) y2s[t] = sm.y2[t];
+            if (tid < C3) {
+                float g4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int m = 0; m < M3; ++m) g4[m & 3] += sm.d3[tid * M3P + m];
+                push(DB3 + tid, OB3 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+            }
+        } else
         // conv3 weight gradient G[o][k] = sum_m d3[o][m] y2col[m][k], pushed.
         // Maps 0..95 on 32x32x2 tiles: element r of a tile holds maps
         // 8(r/4) + r%4 and that + 4 at 32 consecutive k, so a push
