@@ -98,6 +98,35 @@ def test_grad_sum_ragged_batch(chaos, torch_cuda, name, n):
     assert_close(gsum.cpu().numpy(), G, what="grad_sum")
 
 
+def test_batched_grad_sum_several_chunks(chaos, torch_cuda):
+    """The large net's gradient sum contracts its conv3 and FC1 weight
+    gradients over the batch in chunks of samples (64 at this size); 140
+    samples make three chunks, the last one ragged.  Against the per-sample
+    gradients of the unbatched path summed in fp64, and against the oracle
+    (a sample whose max-pool near-tie the fp32 kernel resolves differently is
+    taken out of both sums, as in the per-sample test)."""
+    torch = torch_cuda
+    net, layers, p = _net(chaos, "large")
+    n = 140
+    x, y = wl.batch_set(n)
+    xd, yd = _dev(torch, x, torch.float32), _dev(torch, y, torch.int32)
+    gsum = torch.empty(net.n_params, device="cuda")
+    net.forward_backward(xd, yd, grad_sum=gsum)
+    each = torch.empty(n, net.n_params, device="cuda")
+    net.forward_backward(xd, yd, grad_each=each)
+    torch.cuda.synchronize()
+    g = gsum.cpu().double().numpy()
+    e = each.cpu().double().numpy()
+    assert_close(g, e.sum(0), what="grad_sum against the summed per-sample gradients")
+    refs = [orc.forward_backward(layers, p, x[i], int(y[i])) for i in range(n)]
+    skip = [i for i, r in enumerate(refs)
+            if r["min_gap"] < NEAR_TIE and not close_report(e[i], r["grad"])[0]]
+    assert len(skip) <= 2, f"near-tie samples {skip}"
+    keep = [i for i in range(n) if i not in skip]
+    G = np.sum([refs[i]["grad"] for i in keep], axis=0)
+    assert_close(g - e[skip].sum(0), G, what=f"grad_sum, {n} samples ({len(skip)} near-tie left out)")
+
+
 @pytest.mark.parametrize("name", ["small", "medium", "large", "large_table1"])
 def test_grad_sum_bitwise_reproducible(chaos, torch_cuda, name):
     torch = torch_cuda
