@@ -107,7 +107,11 @@ int chaos_set_params(chaos_net *net, const float *src_dev, hipStream_t stream);
  *   grad_sum_dev   [n_params]      sum_i dE_i/dW, accumulated in a fixed
  *                                  order: bitwise reproducible run to run
  *   grad_each_dev  [n][n_params]   per-sample gradients
- * n = 0 writes zeros into grad_sum_dev and nothing else. */
+ * n = 0 writes zeros into grad_sum_dev and nothing else.  A gradient sum
+ * uses net-owned partial sums allocated on first use (grown when a call
+ * needs more); for the large net without grad_each_dev also 47.6 KB per
+ * sample of per-sample operands, whose conv3 and FC1 weight gradients are
+ * then contracted over the batch (CHAOS_ENOMEM if they cannot be had). */
 int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *labels_dev,
                            int64_t n, float *out_dev, float *loss_dev, float *grad_sum_dev,
                            float *grad_each_dev, hipStream_t stream);
