@@ -33,10 +33,13 @@ constexpr int NT = 256;
 // the next sample's are read from HBM and written to the other buffer while
 // this one's matrix instructions run.
 constexpr int BN3 = 128, RP3 = 128;
+// row stride of the transposed deltas in LDS: the staging writes go down a
+// column (consecutive m), and an odd stride spreads them over the banks
+constexpr int RS3 = RP3 + 1;
 constexpr int NB3 = (KC3 + BN3 - 1) / BN3;  // 17 column blocks
 
 struct alignas(16) Smem3 {
-    float a[2][M3][RP3];  // a[buf][m][o]: zero for o >= C3
+    float a[2][M3][RS3];  // a[buf][m][o]: zero for C3 <= o < RP3
     float b[2][M3][BN3];  // b[buf][m][j]: zero for k0 + j >= KC3
     int koff[BN3];
 };
