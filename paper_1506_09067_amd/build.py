@@ -2,8 +2,11 @@
 from __future__ import annotations
 
 import os
+import shutil
 import subprocess
 import sys
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
@@ -13,7 +16,7 @@ SOURCES = ["worker.hip", "fused_large.hip", "fused_t1.hip", "fused_cpcp.hip", "b
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     # packed fp32 instructions stay disabled in every HIP build
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # no implicit multiply-add contraction: every fused multiply-add in the
@@ -23,20 +26,38 @@ FLAGS = [
 ]
 
 
-def build_library(verbose: bool = False) -> str:
-    """Compile every HIP source into libchaos.so (always recompiles)."""
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, *FLAGS, *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
+    noise = [ln for ln in r.stderr.splitlines() if ln.strip() and "packed-fp32-ops" not in ln]
     if r.returncode != 0:
         sys.stderr.write(r.stdout + r.stderr)
-        raise RuntimeError("hipcc failed building libchaos.so")
-    noise = [ln for ln in r.stderr.splitlines() if ln.strip() and "packed-fp32-ops" not in ln]
-    if verbose and noise:
+    elif verbose and noise:
         sys.stderr.write("\n".join(noise) + "\n")
-    os.replace(tmp, LIB)
+    return r.returncode
+
+
+def build_library(verbose: bool = False, jobs: int | None = None) -> str:
+    """Compile every HIP source into libchaos.so (always recompiles): one
+    object per source, compiled concurrently, then one link."""
+    tmpdir = tempfile.mkdtemp(prefix="chaos_build_")
+    try:
+        objs = [os.path.join(tmpdir, os.path.splitext(s)[0] + ".o") for s in SOURCES]
+        cmds = [[HIPCC, *FLAGS, "-c", os.path.join(CSRC, s), "-o", o]
+                for s, o in zip(SOURCES, objs)]
+        jobs = jobs or min(len(cmds), max(1, min(os.cpu_count() or 1, 16)))
+        with ThreadPoolExecutor(max_workers=jobs) as ex:
+            rcs = list(ex.map(lambda c: _run(c, verbose), cmds))
+        for s, rc in zip(SOURCES, rcs):
+            if rc != 0:
+                raise RuntimeError("hipcc failed compiling %s" % s)
+        tmp = LIB + ".tmp%d" % os.getpid()
+        if _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp], verbose):
+            raise RuntimeError("hipcc failed linking libchaos.so")
+        os.replace(tmp, LIB)
+    finally:
+        shutil.rmtree(tmpdir, ignore_errors=True)
     return LIB
 
 
