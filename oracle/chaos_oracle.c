@@ -461,10 +461,13 @@ int orc_train_sequential(int in_h, int in_w, const int *layers, int n_layers, in
 }
 
 /* Frozen-weight gradient sum G = sum_i grad E_i(W) over x[0..n), accumulated
- * in double in sample order.  loss_out (optional) per-sample loss. */
+ * in double in sample order.  loss_out (optional) per-sample loss; gap_out
+ * (optional) per sample the smallest positive relative max-pool gap of its
+ * forward pass (a diagnostic for the comparison with fp32 results; it does
+ * not enter the sum). */
 int orc_grad_sum(int in_h, int in_w, const int *layers, int n_layers, int act,
                  const double *params, long long n_params, const float *x, const int *labels,
-                 long long n, double *grad_sum, double *loss_out)
+                 long long n, double *grad_sum, double *loss_out, double *gap_out)
 {
     orc_net net;
     int rc = build_net(in_h, in_w, layers, n_layers, &net);
@@ -478,9 +481,11 @@ int orc_grad_sum(int in_h, int in_w, const int *layers, int n_layers, int act,
     if (!g) { ws_free(&ws); return ORC_ENOMEM; }
     memset(grad_sum, 0, (size_t)net.n_params * sizeof(double));
     for (long long i = 0; i < n; ++i) {
-        forward(&net, act, params, x + i * net.in_size, &ws, NULL);
+        double gap = INFINITY;
+        forward(&net, act, params, x + i * net.in_size, &ws, &gap);
         double E = loss_and_top_error(&net, &ws, labels[i], ws.e0);
         if (loss_out) loss_out[i] = E;
+        if (gap_out) gap_out[i] = gap;
         backward(&net, act, (double *)params, 0.0, 0, &ws, g);
         for (long long p = 0; p < net.n_params; ++p) grad_sum[p] += g[p];
     }

@@ -55,7 +55,7 @@ def lib():
         L.orc_conv_backdata.restype = None
         L.orc_forward_backward.argtypes = [i32, i32, P, i32, i32, P, i64, P, i32, P, P, P, P]
         L.orc_train_sequential.argtypes = [i32, i32, P, i32, i32, P, i64, i32, P, P, i64, f64, P, P]
-        L.orc_grad_sum.argtypes = [i32, i32, P, i32, i32, P, i64, P, P, i64, P, P]
+        L.orc_grad_sum.argtypes = [i32, i32, P, i32, i32, P, i64, P, P, i64, P, P, P]
         L.orc_evaluate.argtypes = [i32, i32, P, i32, i32, P, i64, P, P, i64, P, P]
         for name in ("orc_shape", "orc_forward_backward", "orc_train_sequential",
                      "orc_grad_sum", "orc_evaluate"):
@@ -174,8 +174,9 @@ def train_sequential(layers, params, x, labels, lr, act=ACT_TANH, store_f32=True
     return (p, losses, gaps) if with_gaps else (p, losses)
 
 
-def grad_sum(layers, params, x, labels, act=ACT_TANH, in_h=29, in_w=29):
-    """sum_i grad E_i(W) at fixed W (double) -> (G, per-sample losses)."""
+def grad_sum(layers, params, x, labels, act=ACT_TANH, in_h=29, in_w=29, with_gaps=False):
+    """sum_i grad E_i(W) at fixed W (double) -> (G, per-sample losses[, per-sample
+    smallest relative max-pool gaps])."""
     ly = _layers(layers)
     p = _params(params)
     x = np.ascontiguousarray(x, dtype=np.float32)
@@ -183,10 +184,11 @@ def grad_sum(layers, params, x, labels, act=ACT_TANH, in_h=29, in_w=29):
     n = len(labels)
     g = np.zeros(p.size)
     losses = np.zeros(n)
+    gaps = np.zeros(n) if with_gaps else None
     rc = lib().orc_grad_sum(in_h, in_w, _ptr(ly), len(ly) // 3, act, _ptr(p), p.size, _ptr(x),
-                            _ptr(labels), n, _ptr(g), _ptr(losses))
+                            _ptr(labels), n, _ptr(g), _ptr(losses), _ptr(gaps))
     _check(rc, "grad_sum")
-    return g, losses
+    return (g, losses, gaps) if with_gaps else (g, losses)
 
 
 def evaluate(layers, params, x, labels, act=ACT_TANH, in_h=29, in_w=29):

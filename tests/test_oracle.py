@@ -372,3 +372,65 @@ def test_small_net_learns_projection_labels():
     _, wrong1 = orc.evaluate(layers, p1, xt, yt)
     assert losses[-1000:].mean() < 0.92 * losses[:1000].mean()
     assert wrong1 < 0.85 * wrong0
+
+
+# --------------------------------------------------------------------------
+# Prediction ties (reading: lowest index among equal maxima; Table II counts
+# depend on it).  All-zero output-layer weights and biases make every output
+# exactly f(0) = 0, so every prediction is class 0.
+def test_prediction_ties_go_to_the_lowest_index():
+    layers = wl.NETS["small"]
+    p = wl.init_params(layers).astype(np.float64)
+    n_fc2 = 10 * 50 + 10
+    p[-n_fc2:] = 0.0
+    x, y = wl.train_set(200)
+    out, wrong = orc.evaluate(layers, p, x, y)
+    assert np.all(out == 0.0)
+    assert wrong == int(np.sum(y != 0)) and 0 < wrong < 200
+    # a tie between two classes above the rest: outputs 3 and 7 share the
+    # largest bias, so every prediction is 3
+    p[-10:] = [0.1, 0.0, 0.2, 0.5, -0.3, 0.1, 0.0, 0.5, 0.2, -0.1]
+    out, wrong = orc.evaluate(layers, p, x, y)
+    assert np.all(out[:, 3] == out[:, 7]) and np.all(out[:, 3] > out[:, [0, 1, 2, 4, 5, 6, 8, 9]].T)
+    assert wrong == int(np.sum(y != 3))
+
+
+# --------------------------------------------------------------------------
+# The max-pool gap diagnostic (smallest positive relative distance between a
+# window's maximum and its runner-up) decides which fp32/fp64 mismatches the
+# GPU comparisons may forgive, so it is pinned on hand-built windows: a
+# pooling layer directly on the image makes each window's values the pixels.
+def _gap_net_and_images():
+    layers = [(orc.MAXPOOL, 0, 2), (orc.FC, 2, 0)]
+    a = np.array([[0.5, 0.4, 0.9, 0.45],     # window (0,0): 0.5 / 0.4   -> 0.2
+                  [0.2, 0.1, 0.3, 0.2],      # window (0,1): 0.9 / 0.45  -> 0.5
+                  [0.3, 0.2, 0.6, 0.6],      # window (1,0): 0.3 / 0.297 -> 0.01
+                  [0.297, 0.0, 0.6, 0.6]],   # window (1,1): exact tie   -> left out
+                 dtype=np.float32)
+    b = np.array([[-0.3, -0.5, 0.7, 0.7],    # window (0,0): -0.3 / -0.5 -> 2/3
+                  [-0.6, -0.9, 0.7, 0.7],    # the other three windows are exact ties
+                  [0.1, 0.1, 0.2, 0.2],
+                  [0.1, 0.1, 0.2, 0.2]], dtype=np.float32)
+    c = np.full((4, 4), 0.25, dtype=np.float32)  # every window an exact tie
+    return layers, np.stack([a.ravel(), b.ravel(), c.ravel()])
+
+
+def test_min_gap_on_hand_built_windows():
+    layers, x = _gap_net_and_images()
+    p = np.linspace(-0.5, 0.5, orc.n_params(layers, 4, 4))
+    f32 = lambda v: float(np.float32(v))  # the image holds fp32 pixels
+    expect = [(f32(0.3) - f32(0.297)) / f32(0.3),
+              (f32(-0.3) - f32(-0.5)) / abs(f32(-0.3)),
+              math.inf]
+    y = np.array([0, 1, 0], dtype=np.int32)
+    for i in range(3):
+        g = orc.forward_backward(layers, p, x[i], int(y[i]), in_h=4, in_w=4)["min_gap"]
+        assert g == pytest.approx(expect[i], rel=1e-12) if math.isfinite(expect[i]) else g == math.inf
+    assert abs(expect[0] - 0.01) < 1e-6 and abs(expect[1] - 2.0 / 3.0) < 1e-7
+    # the training and gradient-sum paths report the same per-sample gaps
+    _, _, gaps = orc.train_sequential(layers, p, x, y, 0.0, in_h=4, in_w=4, with_gaps=True)
+    _, _, gaps2 = orc.grad_sum(layers, p, x, y, in_h=4, in_w=4, with_gaps=True)
+    for gg in (gaps, gaps2):
+        assert gg[0] == pytest.approx(expect[0], rel=1e-12)
+        assert gg[1] == pytest.approx(expect[1], rel=1e-12)
+        assert gg[2] == math.inf
