@@ -320,7 +320,7 @@ def training_session(chaos, wl, torch, name, epochs, lr, decay, seq_epochs):
         b.record()
         torch.cuda.synchronize()
         rows = [{"epoch": e + 1, "train_loss": float(r[0]), "train_wrong": int(r[1]),
-                 "test_wrong": int(r[2]), "test_loss": float(r[3])}
+                 "test_wrong": int(r[2]), "test_loss": float(r[3]), "diverged": bool(r[4])}
                 for e, r in enumerate(st.cpu().tolist())]
         return rows, a.elapsed_time(b) / 1e3, net.max_workers
 

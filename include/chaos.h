@@ -96,7 +96,11 @@ int64_t chaos_num_params(const chaos_net *net);
 int32_t chaos_num_outputs(const chaos_net *net);
 
 /* Copy the shared weights to / from a device buffer of chaos_num_params()
- * floats in the canonical layout, on `stream`. */
+ * floats in the canonical layout, on `stream`.  These are the network
+ * instances' shared weights of Section III-A.1 (one copy that every worker
+ * reads and updates); get is also how the intermediate results of a session
+ * are serialized (the time model's term d, Section III-B), set how a run is
+ * resumed from them.  dst_dev / src_dev: caller-owned, NULL is CHAOS_EINVAL. */
 int chaos_get_params(const chaos_net *net, float *dst_dev, hipStream_t stream);
 int chaos_set_params(chaos_net *net, const float *src_dev, hipStream_t stream);
 
@@ -116,7 +120,13 @@ int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *la
                            int64_t n, float *out_dev, float *loss_dev, float *grad_sum_dev,
                            float *grad_each_dev, hipStream_t stream);
 
-/* W <- W - lr * grad_dev (n_params floats, canonical layout). */
+/* The weight update of Section II-A: each weight moves against its partial
+ * derivative of the error, scaled by the factor the paper calls the decay
+ * (lambda) and this library the learning rate: W <- W - lr * grad_dev.
+ * grad_dev: n_params floats, canonical layout, caller-owned (for example a
+ * gradient sum from chaos_forward_backward, which makes one step of
+ * mini-batch SGD); NULL is CHAOS_EINVAL.  Each weight is rounded to fp32 once
+ * (one fused multiply-add). */
 int chaos_apply_update(chaos_net *net, const float *grad_dev, float lr, hipStream_t stream);
 
 /* One Training pass over x[0..n) (Section III-A.1 "Training"): each worker
@@ -150,29 +160,40 @@ int chaos_evaluate(chaos_net *net, const float *x_dev, const int32_t *labels_dev
  * Training over x_train[0..n_train) (as chaos_train_epoch, with
  * lr = lr0 * decay^e computed in double and rounded to float), then
  * Validation on the training set and Testing on x_test[0..n_test) (forward
- * only, as chaos_evaluate).  stats_dev [epochs][4] floats receives per epoch:
+ * only, as chaos_evaluate).  stats_dev [epochs][5] floats receives per epoch:
  *   [0] mean training loss (each sample's loss when it was processed)
  *   [1] wrong predictions on the training set after the epoch (Validation)
  *   [2] wrong predictions on the test set (Testing, the Table II count)
  *   [3] mean test loss
+ *   [4] divergence flag: 1 when the epoch's mean test loss (its mean
+ *       training loss if n_test = 0) is not finite or above the mean loss of
+ *       the same set at the session's starting weights, else 0.  A Hogwild
+ *       run whose outputs saturate (the tanh units stuck at +-1.7159) is
+ *       flagged instead of passing silently.
  * ckpt_dev (optional, NULL = skip) [epochs][n_params] receives the weights
  * after each epoch's Training, canonical layout: the per-epoch serialization
  * of intermediate results of the paper's time model (Section III-B, term d).
- * n_test may be 0 (then [2] and [3] are 0).  Uses net-owned buffers of
- * n_train and n_test floats, allocated on first use (the only call here that
- * may allocate device memory after chaos_create_net, together with the batch
- * gradient's partial sums). */
+ * n_test may be 0 (then [2] and [3] are 0).  Before the first epoch one
+ * forward/backward pass at the starting weights over the test set (the
+ * training set if n_test = 0) gives the flag's reference.  Uses net-owned
+ * buffers of max(n_train, n_test) floats, allocated on first use. */
 int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t *labels_train_dev,
                         int64_t n_train, const float *x_test_dev, const int32_t *labels_test_dev,
                         int64_t n_test, int32_t epochs, float lr0, float decay, int32_t mode,
                         int32_t workers, float *stats_dev, float *ckpt_dev, hipStream_t stream);
 
 /* Concurrent Hogwild workers the net's own kernel keeps resident (the
- * default worker count). */
+ * default worker count): the counterpart of the paper's thread count, one
+ * network instance per hardware thread (Section III-A.1; 244 threads on its
+ * Xeon Phi), here one workgroup per in-flight sample.  Negative code on a
+ * NULL net. */
 int32_t chaos_max_workers(const chaos_net *net);
 
 /* Largest accepted worker count: one-wavefront workers of the generic kernel,
- * up to 32 per compute unit (>= chaos_max_workers). */
+ * up to 32 per compute unit (>= chaos_max_workers).  It bounds the thread
+ * count sweep of Section IV-B (the paper runs 1 to 244 threads; the worker
+ * counts above the resident ones are what the performance model of Section
+ * III-C is asked to predict).  Negative code on a NULL net. */
 int32_t chaos_worker_limit(const chaos_net *net);
 
 /* Delayed pushes (a variant of the per-layer update, Section III-A.2, with

@@ -184,14 +184,15 @@ class Net:
     def train_session(self, x, labels, x_test, labels_test, epochs: int, lr0: float,
                       decay: float = 1.0, mode: int = HOGWILD_ATOMIC, workers: int = 0,
                       checkpoints=None):
-        """Training + Validation + Testing per epoch; returns stats [epochs][4] on
+        """Training + Validation + Testing per epoch; returns stats [epochs][5] on
         the device: mean training loss, wrong on the training set, wrong on the
-        test set, mean test loss.  checkpoints: optional float32 CUDA tensor
+        test set, mean test loss, divergence flag (1.0 when the epoch's loss is
+        above the loss at the starting weights).  checkpoints: optional float32 CUDA tensor
         [epochs][n_params] that receives the weights after each epoch's
         Training (canonical layout)."""
         px, py, n = self._xy(x, labels)
         pxt, pyt, nt = self._xy(x_test, labels_test)
-        stats = torch.empty(max(epochs, 1), 4, dtype=torch.float32, device="cuda")
+        stats = torch.empty(max(epochs, 1), 5, dtype=torch.float32, device="cuda")
         ck = _dev(checkpoints, torch.float32, "checkpoints", max(epochs, 0) * self.n_params, True)
         _check(lib().chaos_train_session(self._h, px, py, n, pxt, pyt, nt, int(epochs),
                                          float(lr0), float(decay), int(mode), int(workers),

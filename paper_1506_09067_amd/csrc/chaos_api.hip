@@ -37,7 +37,7 @@ struct chaos_net {
     float *wide_scratch = nullptr;  // [worker_limit][scratch_floats], allocated on first use
     float *sess_loss = nullptr;   // session: per-sample losses (training, then test)
     int64_t sess_loss_n = 0;
-    int32_t *sess_wrong = nullptr;
+    int32_t *sess_wrong = nullptr;  // 64 bytes: [0] wrong count (int32), float [8] reference loss
     float *stash = nullptr;       // large net, batch gradient: per-sample conv3 / FC1 operands
     int64_t stash_n = 0;          // samples the stash holds
     float *bpart = nullptr;       // their chunk partial sums: conv3 rows, then FC1 rows
@@ -568,9 +568,23 @@ int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t 
     }
     if (!net->sess_wrong && hipMalloc(&net->sess_wrong, 64) != hipSuccess)
         return fail(CHAOS_ENOMEM, "session counter");
+    // the divergence flag's reference: the mean loss at the starting weights
+    // on the test set (the training set when there is no test set)
+    float *ref = reinterpret_cast<float *>(net->sess_wrong) + 8;
+    const bool ref_test = n_test > 0;
+    if (epochs > 0) {
+        const float *xr = ref_test ? x_test_dev : x_train_dev;
+        const int32_t *yr = ref_test ? labels_test_dev : labels_train_dev;
+        const int64_t nr = ref_test ? n_test : n_train;
+        int rc = nr > 0 ? chaos_forward_backward(net, xr, yr, nr, nullptr, net->sess_loss, nullptr,
+                                                 nullptr, stream)
+                        : CHAOS_OK;
+        if (rc) return rc;
+        HIP_TRY(chaos::launch_mean(net->sess_loss, nr, ref, stream), "session reference loss");
+    }
     for (int32_t e = 0; e < epochs; ++e) {
         float lr = (float)((double)lr0 * std::pow((double)decay, (double)e));
-        float *st = stats_dev + 4 * (int64_t)e;
+        float *st = stats_dev + 5 * (int64_t)e;
         int rc = chaos_train_epoch(net, x_train_dev, labels_train_dev, n_train, lr, mode, workers,
                                    n_train ? net->sess_loss : nullptr, stream);
         if (rc) return rc;
@@ -590,6 +604,8 @@ int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t 
                                          net->sess_loss, nullptr, nullptr, stream)))
             return rc;
         HIP_TRY(chaos::launch_mean(net->sess_loss, n_test, st + 3, stream), "session mean");
+        HIP_TRY(chaos::launch_above(ref_test ? st + 3 : st + 0, ref, st + 4, stream),
+                "session divergence flag");
     }
     return ok();
 }

@@ -86,6 +86,8 @@ hipError_t launch_axpy_mapped(float *w_dev, const float *g_can, float alpha, con
                               int64_t n_can, hipStream_t s);
 hipError_t launch_mean(const float *v, int64_t n, float *dst, hipStream_t s);
 hipError_t launch_count(const int32_t *src, float *dst, hipStream_t s);
+// dst[0] = 1 if val[0] is not finite or val[0] > ref[0], else 0 (all device scalars)
+hipError_t launch_above(const float *val, const float *ref, float *dst, hipStream_t s);
 // Occupancy of the worker kernel: resident blocks per CU for a given block size.
 int worker_blocks_per_cu(int block);
 

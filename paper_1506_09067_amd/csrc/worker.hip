@@ -171,20 +171,27 @@ __global__ void __launch_bounds__(256) worker_kernel(Net net, WorkArgs a) {
     int64_t step = 0;
 
     for (;; ++step) {
+        // Every wavefront waits for its own pushes of the previous sample to
+        // complete (a workgroup barrier does not wait for them), so after the
+        // barrier below all of this worker's updates have reached memory: the
+        // worker sees its own updates and one worker is exact per-sample SGD.
+        // In frozen mode the same wait keeps the adds into this worker's
+        // partial-sum row in sample order.
+        wait_vector_memory();
         if (train) {
             if (threadIdx.x == 0) s_idx = atomicAdd(a.counter, 1);
-            __syncthreads();
         } else if (threadIdx.x == 0) {
             s_idx = (int64_t)blockIdx.x + step * gridDim.x;
         }
-        if (!train) __syncthreads();
+        __syncthreads();
         const int64_t idx = s_idx;
         __syncthreads();  // everyone has read s_idx before it is rewritten
         if (idx >= a.n) break;
         if (train) {
             // Reads are performed on demand: drop weights cached by this CU
             // during the previous sample so this one sees the pushes made
-            // since (by all workers) at the agent's coherence point.
+            // since (by all workers, this one's included) at the agent's
+            // coherence point.
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             if (a.claims && threadIdx.x == 0) atomicAdd(a.claims + idx, 1);
         }
@@ -307,6 +314,15 @@ __global__ void count_kernel(const int32_t *__restrict__ src, float *__restrict_
     if (threadIdx.x == 0) dst[0] = (float)src[0];
 }
 
+// dst[0] = 1 when *val is not finite or exceeds *ref, else 0
+__global__ void above_kernel(const float *__restrict__ val, const float *__restrict__ ref,
+                             float *__restrict__ dst) {
+    if (threadIdx.x == 0) {
+        const float v = val[0];
+        dst[0] = (isfinite(v) && v <= ref[0]) ? 0.0f : 1.0f;
+    }
+}
+
 __global__ void axpy_kernel(float *__restrict__ w, const float *__restrict__ g, float alpha,
                             int64_t n) {
     int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -386,6 +402,11 @@ hipError_t launch_mean(const float *v, int64_t n, float *dst, hipStream_t s) {
 
 hipError_t launch_count(const int32_t *src, float *dst, hipStream_t s) {
     count_kernel<<<1, 64, 0, s>>>(src, dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_above(const float *val, const float *ref, float *dst, hipStream_t s) {
+    above_kernel<<<1, 64, 0, s>>>(val, ref, dst);
     return hipGetLastError();
 }
 

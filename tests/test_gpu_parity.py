@@ -471,3 +471,67 @@ def test_one_wavefront_workers_beyond_the_fused_capacity(chaos, torch_cuda, name
     net.train_epoch(xd, yd, 1e-3, mode=chaos.HOGWILD_ATOMIC, workers=wmax)
     torch.cuda.synchronize()
     assert torch.isfinite(net.get_params()).all()
+
+
+def test_train_session_against_oracle(chaos, torch_cuda):
+    """The per-epoch driver against the oracle (Section III-A.1: Training,
+    Validation on the training set, Testing; Table II's wrong counts).  Small
+    net, sequential, 500 training and 300 test samples, 3 epochs, lr 1e-3
+    decaying x0.9 per epoch (the small net's schedule) with the library's
+    rounding of each epoch's lr to fp32.
+
+    Epoch e of the oracle starts from the session's own checkpoint of epoch
+    e - 1 (the initial weights for e = 0), so fp32/fp64 differences cannot
+    accumulate over epochs: orc.train_sequential gives the epoch's per-sample
+    losses and weights, orc.evaluate the wrong counts at the session's
+    checkpoint, orc.grad_sum its test losses.  The checkpoint must match at
+    1e-4 unless the epoch contains an ambiguous max-pool tie (gap <
+    AMBIGUOUS, where fp32 and fp64 may route an error differently); then
+    normwise at 1e-3.  The wrong counts are taken at the same weights on both
+    sides and may differ only by predictions whose two largest fp64 outputs
+    are within 1e-5 of the output scale of each other."""
+    torch = torch_cuda
+    layers = wl.NETS["small"]
+    p = wl.init_params(layers)
+    x, y = wl.train_set(500)
+    xt, yt = wl.test_set(300)
+    xd, yd = _dev(torch, x, torch.float32), _dev(torch, y, torch.int32)
+    xtd, ytd = _dev(torch, xt, torch.float32), _dev(torch, yt, torch.int32)
+    lr0, decay, epochs = 1e-3, 0.9, 3
+    net, _, _ = _net(chaos, "small")
+    ckpt = torch.empty(epochs, net.n_params, device="cuda")
+    stats = net.train_session(xd, yd, xtd, ytd, epochs, lr0, decay, mode=chaos.SEQUENTIAL,
+                              checkpoints=ckpt)
+    torch.cuda.synchronize()
+    st, ck = stats.cpu().numpy().astype(np.float64), ckpt.cpu().numpy()
+    lr0f, decayf = float(np.float32(lr0)), float(np.float32(decay))
+
+    def near_ties(out):
+        top2 = np.sort(out, axis=1)[:, -2:]
+        return int(np.sum(top2[:, 1] - top2[:, 0] < 1e-5 * np.max(np.abs(out), axis=1)))
+
+    _, L0 = orc.grad_sum(layers, p, xt, yt)  # the flag's reference: test loss at the start
+    start = p
+    for e in range(epochs):
+        lr = float(np.float32(lr0f * decayf ** e))
+        w, losses, gaps = orc.train_sequential(layers, start, x, y, lr, with_gaps=True)
+        strict = not np.any(gaps < AMBIGUOUS)
+        if strict:
+            assert_close(ck[e], w, what=f"checkpoint of epoch {e}")
+        else:
+            norm = np.max(np.abs(ck[e] - w)) / np.max(np.abs(w))
+            assert norm <= 1e-3, f"checkpoint of epoch {e}, with an ambiguous tie: {norm:.3g}"
+        assert_close(ck[e] - start, w - start, tol=1e-3 if strict else 1e-2,
+                     what=f"weight change of epoch {e}")
+        out_tr, wrong_tr = orc.evaluate(layers, ck[e], x, y)
+        out_te, wrong_te = orc.evaluate(layers, ck[e], xt, yt)
+        _, test_losses = orc.grad_sum(layers, ck[e], xt, yt)
+        assert abs(st[e, 0] - losses.mean()) <= 1e-4 * losses.mean(), (e, st[e, 0], losses.mean())
+        assert abs(st[e, 3] - test_losses.mean()) <= 1e-4 * test_losses.mean(), (e, st[e, 3])
+        assert abs(st[e, 1] - wrong_tr) <= near_ties(out_tr), (e, st[e, 1], wrong_tr)
+        assert abs(st[e, 2] - wrong_te) <= near_ties(out_te), (e, st[e, 2], wrong_te)
+        assert st[e, 4] == float(test_losses.mean() > L0.mean())  # divergence flag
+        print(f"epoch {e}: lr {lr:.6g} strict={strict} loss {st[e, 0]:.6f}/{losses.mean():.6f} "
+              f"wrong {int(st[e, 1])}/{wrong_tr} {int(st[e, 2])}/{wrong_te}", flush=True)
+        start = ck[e]
+    assert st[-1, 0] < st[0, 0] and not st[:, 4].any()
