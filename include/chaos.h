@@ -120,6 +120,27 @@ int chaos_forward_backward(chaos_net *net, const float *x_dev, const int32_t *la
                            int64_t n, float *out_dev, float *loss_dev, float *grad_sum_dev,
                            float *grad_each_dev, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * computation and outputs as chaos_forward_backward, with no hipMalloc,
+ * hipFree or other allocating call.  A gradient sum keeps its per-worker
+ * partial sums in a fixed 32 MiB array of device memory that the library
+ * holds on every device it runs on until the process ends, instead of
+ * net-owned buffers allocated on first use; it therefore runs at most
+ * 32 MiB / (4 n_params) workers (small net 512, medium 110, large 23) and
+ * the large net's conv3 and FC1 gradients are pushed per sample rather than
+ * contracted over the batch.  The sum is bitwise reproducible from call to
+ * call; it equals chaos_forward_backward's to rounding (a different fixed
+ * order), outputs and losses are identical.  A net with more than 8,388,608
+ * weights cannot take a gradient sum here (CHAOS_EUNSUPPORTED).  Every call
+ * on one device shares that array: calls that overlap in time on one device
+ * (different streams, threads or nets) race and give wrong sums; calls
+ * ordered on one stream are safe.  The array is cleared by a kernel at the
+ * start of each call (no memset node when captured). */
+int chaos_forward_backward_noalloc(chaos_net *net, const float *x_dev, const int32_t *labels_dev,
+                                   int64_t n, float *out_dev, float *loss_dev, float *grad_sum_dev,
+                                   float *grad_each_dev, hipStream_t stream);
+
 /* The weight update of Section II-A: each weight moves against its partial
  * derivative of the error, scaled by the factor the paper calls the decay
  * (lambda) and this library the learning rate: W <- W - lr * grad_dev.

@@ -55,6 +55,7 @@ def lib():
             "chaos_get_params": ([P, P, P], ctypes.c_int),
             "chaos_set_params": ([P, P, P], ctypes.c_int),
             "chaos_forward_backward": ([P, P, P, i64, P, P, P, P, P], ctypes.c_int),
+            "chaos_forward_backward_noalloc": ([P, P, P, i64, P, P, P, P, P], ctypes.c_int),
             "chaos_apply_update": ([P, P, f32, P], ctypes.c_int),
             "chaos_train_epoch": ([P, P, P, i64, f32, i32, i32, P, P], ctypes.c_int),
             "chaos_evaluate": ([P, P, P, i64, P, P, P], ctypes.c_int),
@@ -168,6 +169,19 @@ class Net:
     def forward_backward(self, x, labels, out=None, loss=None, grad_sum=None, grad_each=None):
         px, py, n = self._xy(x, labels)
         _check(lib().chaos_forward_backward(
+            self._h, px, py, n,
+            _dev(out, torch.float32, "out", n * self.n_out, True),
+            _dev(loss, torch.float32, "loss", n, True),
+            _dev(grad_sum, torch.float32, "grad_sum", self.n_params, True),
+            _dev(grad_each, torch.float32, "grad_each", n * self.n_params, True),
+            _stream()))
+
+    def forward_backward_noalloc(self, x, labels, out=None, loss=None, grad_sum=None,
+                                 grad_each=None):
+        """chaos_forward_backward_noalloc: as forward_backward, allocating no
+        device memory (partial sums in the library's fixed scratch array)."""
+        px, py, n = self._xy(x, labels)
+        _check(lib().chaos_forward_backward_noalloc(
             self._h, px, py, n,
             _dev(out, torch.float32, "out", n * self.n_out, True),
             _dev(loss, torch.float32, "loss", n, True),

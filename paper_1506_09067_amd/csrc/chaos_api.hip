@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -45,6 +46,14 @@ struct chaos_net {
     int push_delay = 1;           // samples between a worker's pushes (atomic Hogwild)
     int delay_max_workers = 0;    // resident workers of the delayed-push kernel (0 = none)
 };
+
+// Partial-sum rows of chaos_forward_backward_noalloc: a fixed array on every
+// device the library runs on, held until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it is only a stand-in for
+// the symbol): the device address comes from hipGetSymbolAddress, once per
+// device, and is what the kernels receive.
+constexpr int64_t kNoAllocFloats = (int64_t)32 << 18;  // 32 MiB
+static __device__ __align__(256) float scratch[kNoAllocFloats];
 
 namespace {
 
@@ -192,6 +201,27 @@ chaos::WorkArgs base_args(chaos_net *net, const float *x, const int32_t *labels,
     a.counter = net->counter;
     a.push_delay = 1;
     return a;
+}
+
+// Device address of `scratch` on `device` (which must be current), looked up
+// on the first call for that device and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+float *g_scratch_ptr[kMaxDevices] = {};
+
+int noalloc_scratch(int device, float **out) {
+    if (device < 0 || device >= kMaxDevices)
+        return fail(CHAOS_EUNSUPPORTED, "device %d beyond the %d the library tracks", device, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[device]) {
+        void *ptr = nullptr;
+        hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!ptr) return fail(CHAOS_EDEVICE, "hipGetSymbolAddress(scratch) returned NULL");
+        g_scratch_ptr[device] = static_cast<float *>(ptr);
+    }
+    *out = g_scratch_ptr[device];
+    return CHAOS_OK;
 }
 
 hipError_t launch(chaos_net *net, int mode, const chaos::WorkArgs &a, int grid, hipStream_t s) {
@@ -607,6 +637,49 @@ int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t 
         HIP_TRY(chaos::launch_above(ref_test ? st + 3 : st + 0, ref, st + 4, stream),
                 "session divergence flag");
     }
+    return ok();
+}
+
+int chaos_forward_backward_noalloc(chaos_net *net, const float *x_dev, const int32_t *labels_dev,
+                                   int64_t n, float *out_dev, float *loss_dev, float *grad_sum_dev,
+                                   float *grad_each_dev, hipStream_t stream) {
+    if (int rc = check_net(net)) return rc;
+    if (int rc = check_io(x_dev, labels_dev, n)) return rc;
+    if (grad_sum_dev && net->n_params > kNoAllocFloats)
+        return fail(CHAOS_EUNSUPPORTED,
+                    "a gradient sum needs one partial-sum row of %lld floats; the fixed scratch "
+                    "holds %lld",
+                    (long long)net->n_params, (long long)kNoAllocFloats);
+    if (int rc = set_device(net)) return rc;
+    float *rows = nullptr;
+    if (grad_sum_dev) {
+        if (int rc = noalloc_scratch(net->device, &rows)) return rc;
+    }
+    if (n == 0) {
+        if (grad_sum_dev)
+            HIP_TRY(chaos::launch_fill_f32(grad_sum_dev, 0.0f, net->n_params, stream), "zero grad");
+        return ok();
+    }
+    // as chaos_forward_backward: sample i goes to worker i mod grid, each
+    // worker adds its samples' gradients into its own row in sample order,
+    // then the rows are summed in a fixed order; here the grid is bounded by
+    // the rows that fit in the fixed scratch (and the large net's conv3 / FC1
+    // gradients are pushed per sample instead of contracted over the batch,
+    // which would need per-sample operands in memory)
+    int grid = (int)std::min<int64_t>(net->max_workers, n);
+    if (grad_sum_dev) grid = (int)std::min<int64_t>({(int64_t)grid, 512, kNoAllocFloats / net->n_params});
+    chaos::WorkArgs a = base_args(net, x_dev, labels_dev, n);
+    a.out = out_dev;
+    a.loss = loss_dev;
+    a.grad_each = grad_each_dev;
+    a.grad_part = rows;
+    if (grad_sum_dev)  // the rows hold the previous call's sums: clear them (a kernel, no memset node)
+        HIP_TRY(chaos::launch_fill_f32(rows, 0.0f, (int64_t)grid * net->n_params, stream),
+                "zero partial sums");
+    HIP_TRY(launch(net, chaos::kForwardBackward, a, grid, stream), "forward_backward launch");
+    if (grad_sum_dev)
+        HIP_TRY(chaos::launch_reduce_partials(rows, grid, net->n_params, grad_sum_dev, stream),
+                "reduce");
     return ok();
 }
 
