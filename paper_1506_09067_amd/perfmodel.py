@@ -70,7 +70,7 @@ class Model:
     s: float = PEAK_FP32_PER_CU   # FLOP/s of one processing unit
     penalty_train: float = 1.0    # CPI * OperationFactor of a training step
     penalty_fwd: float = 1.0      # the same for a forward pass
-    prep: float = 0.0             # sequential preparation, seconds
+    prep: float = 0.0             # Prep: operations of the sequential preparation
     contention: dict = field(default_factory=dict)  # p -> MemoryContention(p), s per round
 
     def t_train(self):
@@ -99,11 +99,19 @@ class Model:
                 return (1 - w) * self.contention[lo] + w * self.contention[hi]
         raise AssertionError("unreachable")
 
+    def t_seq(self, i, it, ep):
+        """Row (2): the sequential operations (Prep + 4 i + 2 it + 10 ep) / s
+        under the training penalty.  On the GPU Prep is 0 (the weights are
+        drawn by the caller) and the rest is a few microseconds, but the term
+        is kept as the paper states it."""
+        return (self.prep + 4 * i + 2 * it + 10 * ep) / self.s * self.penalty_train
+
     def t_comp(self, i, it, ep, p, validate=True):
-        """Rows (2)-(6) without T_mem: Training, Validation (optional) and
-        Testing over ep epochs with p workers."""
+        """Rows (2)-(6) without T_mem: the sequential operations, then
+        Training, Validation (optional) and Testing over ep epochs with p
+        workers."""
         pi, pit = min(p, i), min(p, it)
-        t = self.prep
+        t = self.t_seq(i, it, ep)
         t += self.t_train() * (i / pi) * ep
         if validate:
             t += self.t_fwd() * (i / pi) * ep
