@@ -167,14 +167,6 @@ def cpu_batch_baseline(layers, p0, x, y, budget_s=3.0):
                       f"in order), {dt:.1f} s"}
 
 
-# Hogwild workers of each net's training row: every resident worker, except
-# the small net, whose 6,405 densely updated weights make 512 and 768
-# concurrent workers spike early in the first epoch and, in a few runs in a
-# hundred, saturate for good; 256 is the largest count its acceptance test
-# passes without a spike.
-ROW_WORKERS = {"small": 256}
-
-
 def mean_test_loss(net, torch, xtd, ytd):
     """Mean loss over the test set at the net's current weights."""
     loss = torch.empty(ytd.numel(), device="cuda")
@@ -192,11 +184,12 @@ def row_quality(initial, final):
 
 def train_row(chaos, wl, torch, name, xd, yd, x, y, xtd, ytd, steps, with_cpu):
     """Training throughput of one net over the resident training set (atomic
-    pushes, lr 1e-3, ROW_WORKERS), and the test loss before and after."""
+    pushes, lr 1e-3, the library's default worker count: one worker per
+    compute unit), and the test loss before and after."""
     layers = wl.NETS[name]
     p0 = wl.init_params(layers)
     net = chaos.Net(layers, p0)
-    workers = ROW_WORKERS.get(name, net.max_workers)
+    workers = net.default_workers
     flops, _ = train_flops_per_sample(layers)
     n = yd.numel()
     initial = mean_test_loss(net, torch, xtd, ytd)
@@ -402,7 +395,7 @@ def delay_sweep(chaos, wl, torch, epochs=5, lr=1e-3, decay=0.9):
 
     def quality(net, mode, lr=lr):
         for e in range(epochs):
-            net.train_epoch(xd, yd, lr * decay ** e, mode=mode)
+            net.train_epoch(xd, yd, lr * decay ** e, mode=mode, workers=net.max_workers)
         loss = torch.empty(10000, device="cuda")
         net.forward_backward(xtd, ytd, loss=loss)
         wrong = net.evaluate(xtd, ytd)
@@ -415,12 +408,12 @@ def delay_sweep(chaos, wl, torch, epochs=5, lr=1e-3, decay=0.9):
     for k in (1, 2, 4, 8, 16, 32, 64):
         net = chaos.Net(layers, p0)
         net.set_push_delay(k)
-        net.train_epoch(xd, yd, lr)
+        net.train_epoch(xd, yd, lr, workers=net.max_workers)
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         for _ in range(2):
-            net.train_epoch(xd, yd, lr)
+            net.train_epoch(xd, yd, lr, workers=net.max_workers)
         b.record()
         torch.cuda.synchronize()
         sps = 2 * 60000 / (a.elapsed_time(b) / 1e3)
@@ -522,7 +515,7 @@ def main():
     initial_test_loss = mean_test_loss(net, torch, xtd, ytd)
     mode = {"atomic": chaos.HOGWILD_ATOMIC, "racy": chaos.HOGWILD_RACY,
             "sequential": chaos.SEQUENTIAL}[args.mode]
-    workers = args.workers or ROW_WORKERS.get(args.net, net.max_workers)
+    workers = args.workers or net.default_workers
     if mode == chaos.SEQUENTIAL:
         workers = 1
     flops, fwd_flops = train_flops_per_sample(layers)

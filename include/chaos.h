@@ -157,7 +157,7 @@ int chaos_apply_update(chaos_net *net, const float *grad_dev, float lr, hipStrea
  * computed, that layer's shared weights receive W <- W - lr * g (Controlled
  * Hogwild, III-A.2) with no synchronisation between workers (Arbitrary Order
  * of Synchronization, III-A.3).  workers: number of concurrent workers for
- * the Hogwild modes (0 = chaos_max_workers(net)); ignored by
+ * the Hogwild modes (0 = chaos_default_workers(net)); ignored by
  * CHAOS_SEQUENTIAL.  Up to chaos_max_workers() the net's own kernel runs,
  * and the workers of an epoch join as its first samples complete (worker b
  * claims its first sample after b/4 samples have been completed), so that
@@ -203,12 +203,24 @@ int chaos_train_session(chaos_net *net, const float *x_train_dev, const int32_t 
                         int64_t n_test, int32_t epochs, float lr0, float decay, int32_t mode,
                         int32_t workers, float *stats_dev, float *ckpt_dev, hipStream_t stream);
 
-/* Concurrent Hogwild workers the net's own kernel keeps resident (the
- * default worker count): the counterpart of the paper's thread count, one
+/* Concurrent Hogwild workers the net's own kernel keeps resident: the
+ * counterpart of the paper's thread count, one
  * network instance per hardware thread (Section III-A.1; 244 threads on its
  * Xeon Phi), here one workgroup per in-flight sample.  Negative code on a
  * NULL net. */
 int32_t chaos_max_workers(const chaos_net *net);
+
+/* The worker count of chaos_train_epoch(workers = 0): one worker per compute
+ * unit, at most chaos_max_workers().  Hogwild's updates are computed at
+ * weights that miss the updates of every other sample in flight, and a net
+ * whose every weight is touched by every sample (the small net of Table I)
+ * trains stably at lr 1e-3 with 256 samples in flight but not always with
+ * 512-768 (its early loss spikes and, in a few runs in a hundred, the tanh
+ * outputs saturate for good); one sample per compute unit is the
+ * concurrency at which every net here passes its acceptance.  Larger counts
+ * up to chaos_max_workers() stay available explicitly.  Negative code on a
+ * NULL net. */
+int32_t chaos_default_workers(const chaos_net *net);
 
 /* Largest accepted worker count: one-wavefront workers of the generic kernel,
  * up to 32 per compute unit (>= chaos_max_workers).  It bounds the thread

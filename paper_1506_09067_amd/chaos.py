@@ -62,6 +62,7 @@ def lib():
             "chaos_train_session": ([P, P, P, i64, P, P, i64, i32, f32, f32, i32, i32, P, P, P],
                                     ctypes.c_int),
             "chaos_max_workers": ([P], ctypes.c_int32),
+            "chaos_default_workers": ([P], ctypes.c_int32),
             "chaos_worker_limit": ([P], ctypes.c_int32),
             "chaos_set_claim_counter": ([P, P], ctypes.c_int),
             "chaos_set_push_delay": ([P, i32], ctypes.c_int),
@@ -141,6 +142,11 @@ class Net:
     @property
     def max_workers(self) -> int:
         return int(lib().chaos_max_workers(self._h))
+
+    @property
+    def default_workers(self) -> int:
+        """Workers of a Hogwild epoch called with workers=0 (one per compute unit)."""
+        return int(lib().chaos_default_workers(self._h))
 
     @property
     def worker_limit(self) -> int:

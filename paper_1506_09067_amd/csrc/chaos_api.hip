@@ -29,6 +29,7 @@ struct chaos_net {
     bool t1 = false;              // the fused kernel of Table I's large net serves this net
     int cpcp = 0;                 // fused small (1) / medium (2) kernel serves this net
     int max_workers = 0;          // resident workers of the training kernel
+    int cus = 0;                  // compute units of the device
     float *scratch = nullptr;     // [max_workers][scratch_floats]
     int32_t *counter = nullptr;   // [0] samples claimed, [1] samples completed (training)
     int fb_workers = 0;           // rows of grad_part
@@ -267,6 +268,7 @@ int chaos_create_net(int32_t in_h, int32_t in_w, const chaos_layer *layers, int3
                             : chaos::worker_blocks_per_cu(net->block);
     if (per_cu < 1) { delete net; return fail(CHAOS_EDEVICE, "occupancy query failed"); }
     net->max_workers = per_cu * cus;
+    net->cus = cus;
     net->delay_max_workers = net->cpcp ? chaos::fused_cpcp_delay_blocks_per_cu(net->cpcp) * cus : 0;
     net->worker_limit = std::max(net->max_workers, chaos::worker_blocks_per_cu(64) * cus);
     // the fused kernels keep every per-sample value in LDS: no scratch
@@ -344,6 +346,11 @@ int32_t chaos_num_outputs(const chaos_net *net) {
 int32_t chaos_max_workers(const chaos_net *net) {
     if (int rc = check_net(net)) return rc;
     return net->push_delay > 1 ? net->delay_max_workers : net->max_workers;
+}
+
+int32_t chaos_default_workers(const chaos_net *net) {
+    if (int rc = check_net(net)) return rc;
+    return std::min(chaos_max_workers(net), net->cus);
 }
 
 int chaos_set_push_delay(chaos_net *net, int32_t k) {
@@ -429,7 +436,7 @@ int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_
         a.loss = loss_dev;
         a.claims = net->claims;
         a.push_delay = net->push_delay;
-        int grid = (int)std::min<int64_t>(workers == 0 ? net->delay_max_workers : workers, n);
+        int grid = (int)std::min<int64_t>(workers == 0 ? chaos_default_workers(net) : workers, n);
         HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 2, stream), "counter reset");
         HIP_TRY(launch(net, chaos::kTrainAtomic, a, grid, stream), "train launch");
         return ok();
@@ -476,7 +483,7 @@ int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_
     int grid = 1;
     int kmode = chaos::kTrainAtomic;
     if (mode != CHAOS_SEQUENTIAL) {
-        grid = workers == 0 ? net->max_workers : workers;
+        grid = workers == 0 ? chaos_default_workers(net) : workers;
         if (mode == CHAOS_HOGWILD_RACY) kmode = chaos::kTrainRacy;
     }
     grid = (int)std::min<int64_t>(grid, n);

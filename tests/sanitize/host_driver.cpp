@@ -80,6 +80,7 @@ int main() {
     CHECK(chaos_num_params(nullptr) == CHAOS_EINVAL);
     CHECK(chaos_num_outputs(nullptr) == CHAOS_EINVAL);
     CHECK(chaos_max_workers(nullptr) == CHAOS_EINVAL);
+    CHECK(chaos_default_workers(nullptr) == CHAOS_EINVAL);
     CHECK(chaos_worker_limit(nullptr) == CHAOS_EINVAL);
     CHECK(chaos_get_params(nullptr, &f, nullptr) == CHAOS_EINVAL);
     CHECK(chaos_set_params(nullptr, &f, nullptr) == CHAOS_EINVAL);

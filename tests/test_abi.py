@@ -80,6 +80,7 @@ def test_null_and_range_arguments(lib):
     # calls on a NULL net
     assert lib.chaos_num_params(None) == -1
     assert lib.chaos_max_workers(None) == -1
+    assert lib.chaos_default_workers(None) == -1
     assert lib.chaos_train_epoch(None, None, None, 0, 0.0, 0, 0, None, None) == -1
     assert lib.chaos_forward_backward(None, None, None, 0, None, None, None, None, None) == -1
     assert lib.chaos_evaluate(None, None, None, 0, None, None, None) == -1

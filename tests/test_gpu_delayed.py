@@ -78,7 +78,7 @@ def test_every_worker_lr_zero_claims_once(env):
     claims = torch.zeros(n, dtype=torch.int32, device="cuda")
     net.set_claim_counter(claims)
     loss = torch.empty(n, device="cuda")
-    net.train_epoch(xd, yd, 0.0, mode=chaos.HOGWILD_ATOMIC, loss=loss)
+    net.train_epoch(xd, yd, 0.0, mode=chaos.HOGWILD_ATOMIC, workers=wmax, loss=loss)
     net.set_claim_counter(None)
     torch.cuda.synchronize()
     assert torch.all(claims == 1)
@@ -87,7 +87,7 @@ def test_every_worker_lr_zero_claims_once(env):
                     for i in range(0, n, n // 16)])
     assert_close(loss.cpu().numpy()[::n // 16], ref, what="losses at lr 0")
     # and a real epoch stays finite and changes the weights
-    net.train_epoch(xd, yd, 1e-3, mode=chaos.HOGWILD_ATOMIC)
+    net.train_epoch(xd, yd, 1e-3, mode=chaos.HOGWILD_ATOMIC, workers=wmax)
     w = net.get_params()
     torch.cuda.synchronize()
     assert torch.isfinite(w).all() and not torch.equal(w.cpu(), torch.from_numpy(p))

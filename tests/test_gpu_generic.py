@@ -149,7 +149,7 @@ def test_generic_every_worker_lr_zero_claims_once(chaos, torch_cuda, name):
     claims = torch.zeros(n, dtype=torch.int32, device="cuda")
     net.set_claim_counter(claims)
     loss = torch.empty(n, device="cuda")
-    net.train_epoch(xd, yd, 0.0, mode=chaos.HOGWILD_ATOMIC, workers=0, loss=loss)
+    net.train_epoch(xd, yd, 0.0, mode=chaos.HOGWILD_ATOMIC, workers=net.max_workers, loss=loss)
     net.set_claim_counter(None)
     torch.cuda.synchronize()
     assert torch.all(claims == 1)

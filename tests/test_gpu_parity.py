@@ -243,7 +243,7 @@ def test_lr_zero_and_claims_once(chaos, torch_cuda, mode, name):
     claims = torch.zeros(n, dtype=torch.int32, device="cuda")
     net.set_claim_counter(claims)
     loss = torch.empty(n, device="cuda")
-    net.train_epoch(xd, yd, 0.0, mode=getattr(chaos, mode), workers=0, loss=loss)
+    net.train_epoch(xd, yd, 0.0, mode=getattr(chaos, mode), workers=net.max_workers, loss=loss)
     net.set_claim_counter(None)
     w = net.get_params()
     ref_loss = torch.empty(n, device="cuda")
