@@ -763,174 +763,199 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                         }
                     }
         };
-        if constexpr (S::C1 % 4 == 0) {
-            // Input maps in blocks of 4, a block owned by one wavefront.  Row
-            // q of tile i holds map c0 + q/4 at uv = 4i + q%4, so the four
-            // lane groups of an accumulator element hold four different maps
-            // at one (u,v): a scatter instruction never has two lanes on one
-            // address, and wave_lds_order() keeps the overlapping groups in
-            // order (plain read-add-write, no atomics).  Seven row tiles per
-            // block, computed in passes of four and three.
-            auto block4 = [&](const int c0) {
+        // Input maps in blocks of 4, a block owned by one wavefront.  Row q of
+        // tile i holds map c0 + q/4 at uv = 4i + q%4, so the four lane groups
+        // of an accumulator element hold four different maps at one (u,v): a
+        // scatter instruction never has two lanes on one address, and
+        // wave_lds_order() keeps the overlapping groups in order (plain
+        // read-add-write, no atomics).  Seven row tiles per block.
+        // (passes of four tiles; of two for the small net, whose three
+        // workers per CU have a third of the registers)
+        auto block4 = [&](const int c0) {
+            constexpr int TI = S::STAGE ? 2 : 4, NPASS = (7 + TI - 1) / TI;
 #pragma unroll
-                for (int pass = 0; pass < 2; ++pass) {
-                    constexpr int TI = 4;
-                    const int i0 = 4 * pass, nt = pass == 0 ? 4 : 3;
-                    f4 acc[TI][RT2];
+            for (int pass = 0; pass < NPASS; ++pass) {
+                const int i0 = TI * pass, nt = (7 - i0 < TI) ? 7 - i0 : TI;
+                f4 acc[TI][RT2];
 #pragma unroll
-                    for (int t = 0; t < TI; ++t)
+                for (int t = 0; t < TI; ++t)
 #pragma unroll
-                        for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
-                    int wo[TI];  // offset of this lane's row in a weight row, or -1
+                    for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
+                int wo[TI];  // offset of this lane's row in a weight row, or -1
+#pragma unroll
+                for (int t = 0; t < TI; ++t) {
+                    const int uv = 4 * (i0 + t) + (lr & 3);
+                    wo[t] = (t < nt && uv < 25) ? (c0 + (lr >> 2)) * 25 + uv : -1;
+                }
+                // the next output maps' weights requested while the
+                // current ones compute
+                float aA[TI], aB[TI];
+                auto load_a = [&](float (&av)[TI], int ks) {
+                    const int o = 4 * ks + lg;
+                    const float *w2 = W2 + (o < S::C2 ? o : 0) * S::W2S;
 #pragma unroll
                     for (int t = 0; t < TI; ++t) {
-                        const int uv = 4 * (i0 + t) + (lr & 3);
-                        wo[t] = (t < nt && uv < 25) ? (c0 + (lr >> 2)) * 25 + uv : -1;
+                        const float v = w2[wo[t] >= 0 ? wo[t] : 0];
+                        av[t] = (o < S::C2 && wo[t] >= 0) ? v : 0.0f;
                     }
-                    // the next output maps' weights requested while the
-                    // current ones compute
-                    float aA[TI], aB[TI];
-                    auto load_a = [&](float (&av)[TI], int ks) {
-                        const int o = 4 * ks + lg;
-                        const float *w2 = W2 + (o < S::C2 ? o : 0) * S::W2S;
-#pragma unroll
-                        for (int t = 0; t < TI; ++t) {
-                            const float v = w2[wo[t] >= 0 ? wo[t] : 0];
-                            av[t] = (o < S::C2 && wo[t] >= 0) ? v : 0.0f;
-                        }
-                    };
-                    auto compute = [&](const float (&av)[TI], int ks) {
-                        const int o = 4 * ks + lg;
-                        float bv[RT2];
-#pragma unroll
-                        for (int j = 0; j < RT2; ++j) {
-                            const float v = sm.d2[o * 96 + 16 * j + lr];  // o < C2P: in the buffer
-                            bv[j] = (o < S::C2) ? v : 0.0f;
-                        }
-#pragma unroll
-                        for (int t = 0; t < TI; ++t)
-#pragma unroll
-                            for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
-                    };
-                    load_a(aA, 0);
-                    for (int ks = 0; ks < S::OKS; ks += 2) {
-                        if (ks + 1 < S::OKS) load_a(aB, ks + 1);
-                        compute(aA, ks);
-                        if (ks + 1 < S::OKS) {
-                            if (ks + 2 < S::OKS) load_a(aA, ks + 2);
-                            compute(aB, ks + 1);
-                        }
-                    }
-                    float *dp[RT2];
+                };
+                auto compute = [&](const float (&av)[TI], int ks) {
+                    const int o = 4 * ks + lg;
+                    float bv[RT2];
 #pragma unroll
                     for (int j = 0; j < RT2; ++j) {
-                        const int p = 16 * j + lr;
-                        const int py = p / S::H2, px = p - py * S::H2;
-                        dp[j] = (p < S::NY2) ? sm.e1 + (c0 + lg) * S::NP1 + py * S::Q1 + px : sm.sink;
+                        const float v = sm.d2[o * 96 + 16 * j + lr];  // o < C2P: in the buffer
+                        bv[j] = (o < S::C2) ? v : 0.0f;
                     }
 #pragma unroll
                     for (int t = 0; t < TI; ++t)
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const int uv = 4 * (i0 + t) + r, u = uv / 5, v = uv - 5 * u;
-                            if (t >= nt || uv >= 25) continue;
-                            float c[RT2];
-#pragma unroll
-                            for (int j = 0; j < RT2; ++j) c[j] = acc[t][j][r];
-                            scatter_add<RT2>(dp, u * S::Q1 + v, c);
-                        }
+                        for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
+                };
+                load_a(aA, 0);
+                for (int ks = 0; ks < S::OKS; ks += 2) {
+                    if (ks + 1 < S::OKS) load_a(aB, ks + 1);
+                    compute(aA, ks);
+                    if (ks + 1 < S::OKS) {
+                        if (ks + 2 < S::OKS) load_a(aA, ks + 2);
+                        compute(aB, ks + 1);
+                    }
                 }
-            };
-            if constexpr (S::C1 == 5 * NW) {
-                // five maps per wavefront: a 4-map block and one map alone
-                block4(5 * wave);
-                map1(5 * wave + 4);
-            } else {
-                for (int blk = wave; blk < S::C1 / 4; blk += NW) block4(4 * blk);
+                float *dp[RT2];
+#pragma unroll
+                for (int j = 0; j < RT2; ++j) {
+                    const int p = 16 * j + lr;
+                    const int py = p / S::H2, px = p - py * S::H2;
+                    dp[j] = (p < S::NY2) ? sm.e1 + (c0 + lg) * S::NP1 + py * S::Q1 + px : sm.sink;
+                }
+#pragma unroll
+                for (int t = 0; t < TI; ++t)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const int uv = 4 * (i0 + t) + r, u = uv / 5, v = uv - 5 * u;
+                        if (t >= nt || uv >= 25) continue;
+                        float c[RT2];
+#pragma unroll
+                        for (int j = 0; j < RT2; ++j) c[j] = acc[t][j][r];
+                        scatter_add<RT2>(dp, u * S::Q1 + v, c);
+                    }
             }
-        } else {
-            // wavefront w owns input maps w, w + 4, ...
-            for (int c = wave; c < S::C1; c += NW) map1(c);
-        }
-        __syncthreads();
+        };
 
-        // ---- conv2 weight gradient: G[o][k] = sum_p d2[o][p] p1col[p][k], pushed;
-        //      pool1 backward: delta at each window's maximum ----
-        {
+        // ---- conv2 weight gradient: G[o][k] = sum_p d2[o][p] p1col[p][k],
+        //      pushed, in passes of JW column tiles of 16 k (JW * CT2
+        //      accumulators keep the matrix core busy) ----
+        constexpr int NJT = S::KC2P / 16, JW = 4;
+        static_assert(NJT % JW == 0, "whole passes");
+        // input offset of output position p = 4s + lg (or -1 past the map)
+        auto pb = [&](int s) {
+            const int p = 4 * s + lg, py = p / S::H2, px = p - py * S::H2;
+            return (p < S::NY2) ? py * S::Q1 + px : -1;
+        };
+        auto wgrad_pass = [&](const int jt0, const float (&ad)[S::CT2][21]) {
+            const float *pc[JW];
+            bool kv[JW];
+#pragma unroll
+            for (int b = 0; b < JW; ++b) {
+                const int k = 16 * (jt0 + b) + lr;
+                kv[b] = k < S::KC2;
+                pc[b] = sm.p1 + (kv[b] ? sm.koff2[k] : 0);
+            }
+            f4 acc[JW][S::CT2];
+#pragma unroll
+            for (int b = 0; b < JW; ++b)
+#pragma unroll
+                for (int i = 0; i < S::CT2; ++i) acc[b][i] = f4{0.f, 0.f, 0.f, 0.f};
+            // operands: unconditional LDS reads from a clamped address,
+            // zeroed by a select (no branch between a read and its use)
+#pragma unroll
+            for (int s = 0; s < 21; ++s) {
+                float bv[JW];
+                const int q = pb(s);  // -1 past the map
+#pragma unroll
+                for (int b = 0; b < JW; ++b) {
+                    const float v = pc[b][q >= 0 ? q : 0];
+                    bv[b] = (kv[b] && q >= 0) ? v : 0.0f;
+                }
+#pragma unroll
+                for (int b = 0; b < JW; ++b)
+#pragma unroll
+                    for (int i = 0; i < S::CT2; ++i) acc[b][i] = mfma(ad[i][s], bv[b], acc[b][i]);
+            }
+#pragma unroll
+            for (int b = 0; b < JW; ++b) {
+                if (!kv[b]) continue;
+                const int k = 16 * (jt0 + b) + lr;
+#pragma unroll
+                for (int i = 0; i < S::CT2; ++i)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        int o = 16 * i + 4 * lg + r;
+                        if (o < S::C2) push(S::DW2 + o * S::KC2S + k, S::OW2 + o * S::KC2 + k, acc[b][i][r]);
+                    }
+            }
+        };
+        // Bias gradients are summed by wavefronts (lanes over positions, then a
+        // fixed butterfly) into gb, the FC activations' buffer (free once the
+        // FC gradients are pushed), and pushed together by consecutive
+        // threads: one push instruction per bias block, as for every other
+        // block of weights (single-lane pushes to the same few lines would
+        // queue behind each other at the memory side).
+        float *gb = sm.h;  // [0, C2) conv2 biases, [C2, C2 + C1) conv1 biases
+        static_assert(S::C2 + S::C1 <= S::F1 + 16, "bias sums fit in the FC activations' buffer");
+        // this wavefront's weight-gradient passes (every jt0 = first + step * n)
+        // and the conv2 bias gradients of maps o = ofirst + ostep * n (a map's
+        // deltas summed over its 81 positions)
+        auto conv2_wgrad = [&](const int first, const int step, const int ofirst, const int ostep) {
             float ad[S::CT2][21];
 #pragma unroll
             for (int i = 0; i < S::CT2; ++i)
 #pragma unroll
                 for (int s = 0; s < 21; ++s) ad[i][s] = sm.d2[(16 * i + lr) * 96 + 4 * s + lg];
-            // input offset of output position p = 4s + lg (or -1 past the map)
-            auto pb = [&](int s) {
-                const int p = 4 * s + lg, py = p / S::H2, px = p - py * S::H2;
-                return (p < S::NY2) ? py * S::Q1 + px : -1;
-            };
-            // JB column tiles of 16 k per pass, so that JB * CT2 accumulators
-            // keep the matrix core busy
-            constexpr int NJT = S::KC2P / 16, JB = (NJT / NW >= 4) ? 4 : 2;
-            static_assert(NJT % (NW * JB) == 0, "whole passes");
-            for (int jt0 = wave * JB; jt0 < NJT; jt0 += NW * JB) {
-                const float *pc[JB];
-                bool kv[JB];
-#pragma unroll
-                for (int b = 0; b < JB; ++b) {
-                    const int k = 16 * (jt0 + b) + lr;
-                    kv[b] = k < S::KC2;
-                    pc[b] = sm.p1 + (kv[b] ? sm.koff2[k] : 0);
-                }
-                f4 acc[JB][S::CT2];
-#pragma unroll
-                for (int b = 0; b < JB; ++b)
-#pragma unroll
-                    for (int i = 0; i < S::CT2; ++i) acc[b][i] = f4{0.f, 0.f, 0.f, 0.f};
-                // operands: unconditional LDS reads from a clamped address,
-                // zeroed by a select (no branch between a read and its use)
-#pragma unroll
-                for (int s = 0; s < 21; ++s) {
-                    float bv[JB];
-                    const int q = pb(s);  // -1 past the map
-#pragma unroll
-                    for (int b = 0; b < JB; ++b) {
-                        const float v = pc[b][q >= 0 ? q : 0];
-                        bv[b] = (kv[b] && q >= 0) ? v : 0.0f;
-                    }
-#pragma unroll
-                    for (int b = 0; b < JB; ++b)
-#pragma unroll
-                        for (int i = 0; i < S::CT2; ++i) acc[b][i] = mfma(ad[i][s], bv[b], acc[b][i]);
-                }
-#pragma unroll
-                for (int b = 0; b < JB; ++b) {
-                    if (!kv[b]) continue;
-                    const int k = 16 * (jt0 + b) + lr;
-#pragma unroll
-                    for (int i = 0; i < S::CT2; ++i)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            int o = 16 * i + 4 * lg + r;
-                            if (o < S::C2) push(S::DW2 + o * S::KC2S + k, S::OW2 + o * S::KC2 + k, acc[b][i][r]);
-                        }
-                }
+            for (int jt0 = first; jt0 < NJT; jt0 += step) wgrad_pass(jt0, ad);
+            for (int o = ofirst; o < S::C2; o += ostep) {
+                float g = 0.0f;
+                for (int p = lane; p < S::NY2; p += 64) g += sm.d2[o * 96 + p];
+                g = wave_sum(g);
+                if (lane == 0) gb[o] = g;
             }
-            if (tid < S::C2) {
-                float g4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-                for (int p = 0; p < S::NY2; ++p) g4[p & 3] += sm.d2[tid * 96 + p];
-                push(S::DB2 + tid, S::OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+        };
+        if constexpr (S::STAGE) {
+            // Small net: backward data and weight gradient in one phase.  They
+            // read the same deltas and write different places: backward data
+            // the pool1 errors in LDS, from this sample's LDS copy of the
+            // weights (which the pushes do not touch); the weight gradient the
+            // shared weights.  Wavefront 0 takes input maps 0..3 as a block,
+            // wavefront 1 map 4 alone, wavefronts 2 and 3 the weight
+            // gradient's column tiles and the biases.
+            static_assert(S::C1 == 5 && NJT == 2 * JW, "small net: 5 input maps, two passes");
+            if (wave == 0) block4(0);
+            else if (wave == 1) map1(4);
+            else conv2_wgrad(JW * (wave - 2), 2 * JW, wave - 2, 2);
+        } else {
+            if constexpr (S::C1 == 5 * NW) {
+                // five maps per wavefront: a 4-map block and one map alone
+                block4(5 * wave);
+                map1(5 * wave + 4);
+            } else if constexpr (S::C1 % 4 == 0) {
+                for (int blk = wave; blk < S::C1 / 4; blk += NW) block4(4 * blk);
+            } else {
+                // wavefront w owns input maps w, w + 4, ...
+                for (int c = wave; c < S::C1; c += NW) map1(c);
             }
-            for (int t = tid; t < S::C1 * S::NP1; t += NT) sm.e1[t] *= dact_from_y(sm.p1[t]);
+            conv2_wgrad(JW * wave, NW * JW, wave, NW);
         }
         __syncthreads();
 
         // ---- conv1 weight gradient G[o][uv] = sum over the 26x26 conv1 outputs
-        //      of the delta (nonzero only at each pooling window's maximum)
-        //      times the input under the kernel, on the matrix cores: rows o,
-        //      cols uv = 4u + v, K = 4P + w with the pooled positions P split
-        //      over the wavefronts; the partial tiles are summed in wavefront
-        //      order (through the free delta buffer).  Bias: deltas summed per
-        //      map. ----
+        //      of the delta times the input under the kernel, on the matrix
+        //      cores: rows o, cols uv = 4u + v, K = 4P + w with the pooled
+        //      positions P split over the wavefronts; the partial tiles are
+        //      summed in wavefront order (through the free delta buffer).  The
+        //      delta is nonzero only at each pooling window's maximum, where it
+        //      is the pool1 error times f' of the pool1 value (pool1 backward,
+        //      formed as the operands are read).  Bias: the deltas summed per
+        //      map by one wavefront. ----
         {
             f4 acc[2][S::CT1];
 #pragma unroll
@@ -945,28 +970,50 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 orow[t] = (ov[t] ? 16 * t + lr : 0) * S::NP1;
             }
             const int xo = ((lg >> 1) + (lr >> 2)) * S::IN + (lg & 1) + (lr & 3);
-            auto step = [&](int P, f4 (&c)[S::CT1]) {
+            // operands of pooled position P, read a position ahead of their use
+            auto operands = [&](int P, float &bx, float (&av)[S::CT1]) {
                 const int py = P / S::Q1, px = P - py * S::Q1;
-                const float bx = sm.x[2 * py * S::IN + 2 * px + xo];
+                bx = sm.x[2 * py * S::IN + 2 * px + xo];
 #pragma unroll
                 for (int t = 0; t < S::CT1; ++t) {
                     const int am = sm.am1[orow[t] + P];  // orow 0 when the map is past C1
-                    const float v = sm.e1[orow[t] + P];
-                    const float av = (ov[t] && am == lg) ? v : 0.0f;
-                    c[t] = mfma(av, bx, c[t]);
+                    const float e = sm.e1[orow[t] + P], y = sm.p1[orow[t] + P];
+                    av[t] = (ov[t] && am == lg) ? e * dact_from_y(y) : 0.0f;
                 }
             };
-            int P = wave;
-            for (; P + NW < S::NP1; P += 2 * NW) {
-                step(P, acc[0]);
-                step(P + NW, acc[1]);
+            auto compute = [&](const float bx, const float (&av)[S::CT1], f4 (&c)[S::CT1]) {
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int t = 0; t < S::CT1; ++t) c[t] = mfma(av[t], bx, c[t]);
+            };
+            // acc[0] takes positions wave, wave + 2 NW, ...; acc[1] wave + NW, ...
+            float bxA, bxB, avA[S::CT1], avB[S::CT1];
+            if (wave < S::NP1) operands(wave, bxA, avA);
+            for (int P = wave; P < S::NP1; P += 2 * NW) {
+                const bool q = P + NW < S::NP1;
+                if (q) operands(P + NW, bxB, avB);
+                compute(bxA, avA, acc[0]);
+                if (q) {
+                    if (P + 2 * NW < S::NP1) operands(P + 2 * NW, bxA, avA);
+                    compute(bxB, avB, acc[1]);
+                }
             }
-            if (P < S::NP1) step(P, acc[0]);
+            // the conv2 biases summed in the previous phase; the conv1 biases:
+            // map o by wavefront o % NW, lanes over the pooled positions
+            if (tid < S::C2) push(S::DB2 + tid, S::OB2 + tid, gb[tid]);
+            for (int o = wave; o < S::C1; o += NW) {
+                float g = 0.0f;
+                for (int q = lane; q < S::NP1; q += 64)
+                    g += sm.e1[o * S::NP1 + q] * dact_from_y(sm.p1[o * S::NP1 + q]);
+                g = wave_sum(g);
+                if (lane == 0) gb[S::C2 + o] = g;
+            }
             float *red = sm.d2;  // [wavefront][tile][lane][4]
 #pragma unroll
             for (int t = 0; t < S::CT1; ++t)
                 *(f4 *)(red + ((wave * S::CT1 + t) * 64 + lane) * 4) = acc[0][t] + acc[1][t];
             __syncthreads();
+            // weights and biases of conv1, consecutive in memory, one block
             for (int t = tid; t < S::C1 * 16 + S::C1; t += NT) {
                 if (t < S::C1 * 16) {
                     const int o = t >> 4, uv = t & 15, tile = o >> 4, row = o & 15;
@@ -976,11 +1023,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     for (int w = 1; w < NW; ++w) g += red[(w * S::CT1 + tile) * 256 + e];
                     push(S::DW1 + t, S::OW1 + t, g);
                 } else {
-                    const int o = t - S::C1 * 16;
-                    float g4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-                    for (int q = 0; q < S::NP1; ++q) g4[q & 3] += sm.e1[o * S::NP1 + q];
-                    push(S::DB1 + o, S::OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                    push(S::DB1 + t - S::C1 * 16, S::OB1 + t - S::C1 * 16, gb[S::C2 + t - S::C1 * 16]);
                 }
             }
         }

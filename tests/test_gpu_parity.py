@@ -521,8 +521,12 @@ def test_train_session_against_oracle(chaos, torch_cuda):
         else:
             norm = np.max(np.abs(ck[e] - w)) / np.max(np.abs(w))
             assert norm <= 1e-3, f"checkpoint of epoch {e}, with an ambiguous tie: {norm:.3g}"
-        assert_close(ck[e] - start, w - start, tol=1e-3 if strict else 1e-2,
-                     what=f"weight change of epoch {e}")
+        # the epoch's weight change, normwise (elementwise, a change of 1 % of
+        # the largest one carries the fp32 storage rounding of 500 updates,
+        # about 1e-2 of itself, on both sides)
+        dw, dref = ck[e] - start, w - start
+        assert np.max(np.abs(dw - dref)) <= (1e-3 if strict else 1e-2) * np.max(np.abs(dref)), (
+            f"weight change of epoch {e}: {np.max(np.abs(dw - dref)) / np.max(np.abs(dref)):.3g}")
         out_tr, wrong_tr = orc.evaluate(layers, ck[e], x, y)
         out_te, wrong_te = orc.evaluate(layers, ck[e], xt, yt)
         _, test_losses = orc.grad_sum(layers, ck[e], xt, yt)
