@@ -29,11 +29,8 @@ struct Cpcp {
     static constexpr int NP2 = 9;                       // pool2 output 3x3
     static constexpr int NF1 = C2 * NP2;                // FC1 inputs
     static constexpr int KC2 = C1 * 25;                 // conv2 K = (c,u,v)
-    static constexpr int OW2_ = C1 * 16 + C1;           // offset of the conv2 weights
     static constexpr int KC2P = (KC2 + 15) / 16 * 16;   // padded to whole tiles
     static constexpr int KQ2 = (KC2 + 31) / 32 * 8;     // conv2 forward K padded to 4 KQ2
-    // 16-byte loads of conv2 weight rows need 16-byte aligned row starts
-    static constexpr bool W2_ALIGNED16 = (OW2_ % 4 == 0) && (KC2 % 4 == 0);
     static constexpr int CT1 = (C1 + 15) / 16;          // conv1 col tiles
     static constexpr int CT2 = (C2 + 15) / 16;          // conv2 map tiles
     static constexpr int C2P = CT2 * 16;
@@ -45,18 +42,19 @@ struct Cpcp {
     static constexpr int OF1 = OB2 + C2, OBF1 = OF1 + F1 * NF1;
     static constexpr int OF2 = OBF1 + F1, OBF2 = OF2 + F2 * F1;
     static constexpr int NPARAM = OBF2 + F2;
-    // A weight vector of at most 8K floats (the small net: 25.6 KB) is copied
-    // into LDS once per sample and every later weight read of the sample is
-    // served from there: one round trip to memory per sample instead of one
-    // per layer and pass.
+    // A weight vector of at most 8K floats (the small net: 27.6 KB in its
+    // device layout) is copied into LDS once per sample and every later
+    // weight read of the sample is served from there: one round trip to
+    // memory per sample instead of one per layer and pass.
     static constexpr bool STAGE = NPARAM <= 8192;
-    static constexpr int NPARAM4 = (NPARAM + 3) / 4 * 4;
-    // Device layout of the shared weights.  A net whose vector is not copied
-    // whole (the medium net) starts every segment on a 64-byte boundary and
-    // pads the conv2, FC1 and FC2 rows to multiples of 16 floats (the padding
-    // stays zero), so the pushes of a row cover whole 64-byte segments; the
-    // small net keeps the canonical layout.
-    static constexpr bool PAD = !STAGE;
+    // Device layout of the shared weights: every segment starts on a 64-byte
+    // boundary and the conv2, FC1 and FC2 rows are padded to multiples of 16
+    // floats (the padding stays zero), so the pushes of a row cover whole
+    // 64-byte segments and no segment is shared by two rows.  The memory-side
+    // atomic units process one request per segment and serialize requests to
+    // one line; the small net, whose every line takes a read and an add from
+    // every sample, is bound by exactly that.
+    static constexpr bool PAD = true;
     static constexpr int KC2S = pad16(PAD, KC2), NF1S = pad16(PAD, NF1), F1S = pad16(PAD, F1);
     static constexpr int DW1 = 0, DB1 = C1 * 16;
     static constexpr int DW2 = pad16(PAD, DB1 + C1), DB2 = DW2 + C2 * KC2S;
@@ -64,6 +62,7 @@ struct Cpcp {
     static constexpr int DF2 = pad16(PAD, DBF1 + F1), DBF2 = DF2 + F2 * F1S;
     static constexpr int NDEV = pad16(PAD, DBF2 + F2);
     static_assert(PAD || NDEV == NPARAM, "the unpadded layout is the canonical one");
+    static_assert(NDEV % 4 == 0, "whole 16-byte loads of the device vector");
     // FC1 rows read with 16-byte loads when every row start is 16-byte aligned
     static constexpr int FC1_VEC = (DF1 % 4 == 0 && NF1S % 4 == 0 && NF1 % 4 == 0) ? 4 : 1;
     // Otherwise the conv2 weights (80 KB for the medium net), read by the
@@ -73,6 +72,9 @@ struct Cpcp {
     static constexpr bool STAGE2 = !STAGE && NW2 <= 20480 && DW2 % 4 == 0 && KC2 % 4 == 0;
     // row stride of the conv2 weights as the kernel reads them
     static constexpr int W2S = STAGE2 ? KC2 : KC2S;
+    // 16-byte loads of conv2 weight rows need 16-byte aligned row starts (the
+    // LDS copies are 16-byte aligned; a row's padding reads as zero)
+    static constexpr bool W2_ALIGNED16 = ((STAGE2 ? 0 : DW2) % 4 == 0) && (W2S % 4 == 0);
 };
 
 constexpr int NT = 256, NW = 4;
@@ -93,11 +95,11 @@ struct alignas(16) SmemCpcp {
     alignas(16) int koff2[4 * S::KQ2];   // im2col offset into p1 of k = (c,u,v) (0 past KC2)
     unsigned char am1[S::C1 * S::NP1 + 16];
     unsigned char am2[S::NF1 + 16];
-    alignas(16) float w[S::STAGE ? S::NPARAM4 : 4];  // the weights read at the start of the sample
+    alignas(16) float w[S::STAGE ? S::NDEV : 4];  // the weights read at the start of the sample
     alignas(16) float w2[S::STAGE2 ? S::NW2 : 4];    // the conv2 weights read at the start of the sample
     float sink[64];                      // scatter target of padding lanes
-    // delayed pushes: this worker's gradient sum since its last push
-    alignas(16) float gacc[DELAY ? S::NPARAM4 : 4];
+    // delayed pushes: this worker's gradient sum since its last push (device layout)
+    alignas(16) float gacc[DELAY ? S::NDEV : 4];
     int64_t idx;
 };
 
@@ -110,8 +112,8 @@ struct alignas(16) SmemCpcp {
 // reads.
 template <class S, int MODE, int MINB, bool DELAY = false>
 __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
-    static_assert(!DELAY || (MODE == kTrainAtomic && S::STAGE && !S::PAD),
-                  "delayed pushes: atomic training of a net copied whole into LDS, canonical layout");
+    static_assert(!DELAY || (MODE == kTrainAtomic && S::STAGE),
+                  "delayed pushes: atomic training of a net copied whole into LDS");
     __shared__ SmemCpcp<S, DELAY> sm;
     const float *Wg = a.params;
     // every weight read below goes through W: the LDS copy or the shared vector
@@ -129,7 +131,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
     }
     int nproc = 0;  // samples this worker has processed (delayed pushes)
     if constexpr (DELAY) {
-        for (int i = threadIdx.x; i < S::NPARAM; i += NT) sm.gacc[i] = 0.0f;
+        for (int i = threadIdx.x; i < S::NDEV; i += NT) sm.gacc[i] = 0.0f;
     }
     // pushes this worker's gradient sum (W += -lr * sum, the rounding of the
     // per-layer push) and clears it; after a barrier
@@ -141,7 +143,8 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             fp.neg_lr = -a.lr;
             fp.each = nullptr;
             fp.part = nullptr;
-            for (int i = threadIdx.x; i < S::NPARAM; i += NT) {
+            // the whole device vector, padding included (its sums stay zero)
+            for (int i = threadIdx.x; i < S::NDEV; i += NT) {
                 fp(i, sm.gacc[i]);
                 sm.gacc[i] = 0.0f;
             }
@@ -189,7 +192,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         if constexpr (S::STAGE) {
             // the weights of this sample: all 16-byte loads are issued before
             // the first LDS write (the vector starts 16-byte aligned)
-            constexpr int N4 = S::NPARAM / 4, PER = (N4 + NT - 1) / NT, TAIL = S::NPARAM - 4 * N4;
+            constexpr int N4 = S::NDEV / 4, PER = (N4 + NT - 1) / NT, TAIL = S::NDEV - 4 * N4;
             f4 wv[PER];
 #pragma unroll
             for (int q = 0; q < PER; ++q) {
@@ -510,7 +513,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         // a layer's gradient element (each weight once per sample, by one
         // thread): pushed now, or added to the worker's sum
         auto push = [&](int w_off, int g_off, float g) {
-            if constexpr (DELAY) sm.gacc[g_off] += g;
+            if constexpr (DELAY) sm.gacc[w_off] += g;
             else push_now(w_off, g_off, g);
         };
 

@@ -301,10 +301,10 @@ def test_bad_arguments_are_rejected(chaos, torch_cuda):
     assert e.value.code == chaos.EINVAL
 
 
-@pytest.mark.parametrize("name", ["medium", "large", "large_table1"])
+@pytest.mark.parametrize("name", ["small", "medium", "large", "large_table1"])
 def test_apply_update_and_param_roundtrip(chaos, torch_cuda, name):
-    # the two large nets keep their weights in a padded device layout: get,
-    # set and update convert, so the canonical view must round-trip exactly
+    # every fused net keeps its weights in a padded device layout: get, set
+    # and update convert, so the canonical view must round-trip exactly
     torch = torch_cuda
     net, _, p = _net(chaos, name)
     g = torch.randn(net.n_params, device="cuda")
