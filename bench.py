@@ -18,9 +18,9 @@ Prints one JSON line.  Extra fields:
   cpu_baseline  the CPU oracle (sequential per-sample SGD, one core) on a
                 bounded sample of the same workload
   rows          training throughput of the small and medium nets and of
-                Table I's large net on the same set (every resident worker,
-                with the FP32-peak fraction and the oracle's sequential rate
-                on a short prefix), and the
+                Table I's large net on the same set (default workers, with
+                the FP32-peak fraction and the oracle's sequential rate on a
+                short prefix), of the small net on 8 weight replicas, and the
                 throughput of the frozen-weight 16,384-sample batch gradient
                 and of the 10,000-sample test forward pass of the large net
 """
@@ -182,13 +182,17 @@ def row_quality(initial, final):
             "converging": bool(final == final and final < initial)}
 
 
-def train_row(chaos, wl, torch, name, xd, yd, x, y, xtd, ytd, steps, with_cpu):
+def train_row(chaos, wl, torch, name, xd, yd, x, y, xtd, ytd, steps, with_cpu, replicas=None):
     """Training throughput of one net over the resident training set (atomic
     pushes, lr 1e-3, the library's default worker count: one worker per
-    compute unit), and the test loss before and after."""
+    compute unit), and the test loss before and after.  replicas = (r, m):
+    the workers read r weight replicas refreshed every m samples
+    (chaos_set_replicas)."""
     layers = wl.NETS[name]
     p0 = wl.init_params(layers)
     net = chaos.Net(layers, p0)
+    if replicas:
+        net.set_replicas(*replicas)
     workers = net.default_workers
     flops, _ = train_flops_per_sample(layers)
     n = yd.numel()
@@ -209,6 +213,8 @@ def train_row(chaos, wl, torch, name, xd, yd, x, y, xtd, ytd, steps, with_cpu):
            "tflops": tflops, "frac_fp32_peak": tflops / PEAK_FP32_TFLOPS,
            "ms_per_epoch": a.elapsed_time(b) / steps,
            "quality": row_quality(initial, mean_test_loss(net, torch, xtd, ytd))}
+    if replicas:
+        row["replicas"] = {"copies": replicas[0], "refresh_every": replicas[1]}
     if with_cpu:
         row["cpu_oracle"] = cpu_baseline(layers, p0, x, y, budget_s=3.0)
     return row
@@ -553,6 +559,8 @@ def main():
                 rows[f"train_{name}_{args.samples}"] = train_row(
                     chaos, wl, torch, name, xd, yd, x, y, xtd, ytd, args.steps,
                     not args.no_cpu_baseline)
+        rows[f"train_small_replicas_8x8_{args.samples}"] = train_row(
+            chaos, wl, torch, "small", xd, yd, x, y, xtd, ytd, args.steps, False, replicas=(8, 8))
         xb, yb = wl.batch_set(16384)
         xbd, ybd = torch.from_numpy(xb).cuda(), torch.from_numpy(yb).cuda()
         g = torch.empty(net.n_params, device="cuda")

@@ -243,6 +243,27 @@ int32_t chaos_worker_limit(const chaos_net *net);
  * worker counts are CHAOS_EINVAL. */
 int chaos_set_push_delay(chaos_net *net, int32_t k);
 
+/* Weight replicas (an update-path variant for nets whose every weight is
+ * touched by every sample, Controlled Hogwild's delayed sharing applied to
+ * the reads, Section III-A.2): with r > 1, each worker of a
+ * CHAOS_HOGWILD_ATOMIC epoch reads its weights from replica (worker index
+ * mod r) instead of the shared weights, pushes every update to the shared
+ * weights and to that replica, and the replica is copied from the shared
+ * weights after every m-th sample completed on it.  A worker then sees the
+ * updates of workers on its replica at once and the others' after at most
+ * about r * m further samples.  Every replica equals the shared weights at the
+ * start of each epoch; the shared weights stay the result.  With one worker
+ * this is sequential per-sample SGD bit for bit.  The memory side serializes
+ * requests to one cache line, and every sample reads and adds into every
+ * line of such a net's weights: r replicas spread those requests.  r = 1 (the
+ * default) turns replicas off.  Only the small net of Table I supports r > 1
+ * (its weights fit in LDS), else CHAOS_EUNSUPPORTED; r outside [1, 64] or
+ * m < 1 is CHAOS_EINVAL, as is combining r > 1 with a push delay k > 1.
+ * Allocates r copies of the weights (device memory owned by the net).
+ * CHAOS_SEQUENTIAL and CHAOS_HOGWILD_RACY epochs ignore the setting, as do
+ * worker counts above chaos_max_workers(). */
+int chaos_set_replicas(chaos_net *net, int32_t r, int32_t m);
+
 /* Debug aid: when claims_dev (int32 [n] of the next chaos_train_epoch) is not
  * NULL, every processed sample index i adds 1 to claims_dev[i]; NULL turns it
  * off.  The buffer must hold at least n entries for each later call. */

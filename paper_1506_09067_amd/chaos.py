@@ -66,6 +66,7 @@ def lib():
             "chaos_worker_limit": ([P], ctypes.c_int32),
             "chaos_set_claim_counter": ([P, P], ctypes.c_int),
             "chaos_set_push_delay": ([P, i32], ctypes.c_int),
+            "chaos_set_replicas": ([P, i32, i32], ctypes.c_int),
             "chaos_last_error": ([], ctypes.c_char_p),
         }
         for name, (args, res) in sig.items():
@@ -231,6 +232,12 @@ class Net:
     def set_claim_counter(self, claims):
         _check(lib().chaos_set_claim_counter(
             self._h, _dev(claims, torch.int32, "claims", optional=True)))
+
+    def set_replicas(self, r: int, m: int = 4):
+        """Atomic Hogwild workers read r replicas of the weights, each copied
+        from the shared weights after every m-th sample completed on it
+        (r = 1: off)."""
+        _check(lib().chaos_set_replicas(self._h, int(r), int(m)))
 
     def set_push_delay(self, k: int):
         """Samples between a worker's pushes in atomic Hogwild epochs (1 = per layer)."""

@@ -45,6 +45,10 @@ struct chaos_net {
     float *bpart = nullptr;       // their chunk partial sums: conv3 rows, then FC1 rows
     int64_t bpart_chunks = 0;
     int push_delay = 1;           // samples between a worker's pushes (atomic Hogwild)
+    int n_replicas = 1;           // weight replicas read by the workers (atomic Hogwild)
+    int refresh_every = 1;        // samples per replica between its refreshes
+    float *replicas = nullptr;    // [n_replicas][device floats]
+    int32_t *rep_counter = nullptr;  // [n_replicas]
     int delay_max_workers = 0;    // resident workers of the delayed-push kernel (0 = none)
 };
 
@@ -329,6 +333,8 @@ int chaos_destroy_net(chaos_net *net) {
     (void)hipFree(net->sess_wrong);
     (void)hipFree(net->stash);
     (void)hipFree(net->bpart);
+    (void)hipFree(net->replicas);
+    (void)hipFree(net->rep_counter);
     delete net;
     return ok();
 }
@@ -358,7 +364,37 @@ int chaos_set_push_delay(chaos_net *net, int32_t k) {
     if (k < 1) return fail(CHAOS_EINVAL, "push delay %d < 1", k);
     if (k > 1 && net->delay_max_workers < 1)
         return fail(CHAOS_EUNSUPPORTED, "delayed pushes need a net whose weights fit in LDS");
+    if (k > 1 && net->n_replicas > 1)
+        return fail(CHAOS_EINVAL, "delayed pushes and weight replicas exclude each other");
     net->push_delay = k;
+    return ok();
+}
+
+int chaos_set_replicas(chaos_net *net, int32_t r, int32_t m) {
+    if (int rc = check_net(net)) return rc;
+    if (r < 1 || r > 64) return fail(CHAOS_EINVAL, "replicas %d outside [1,64]", r);
+    if (m < 1) return fail(CHAOS_EINVAL, "refresh interval %d < 1", m);
+    if (r > 1 && !(net->cpcp && chaos::fused_cpcp_supports_replicas(net->cpcp)))
+        return fail(CHAOS_EUNSUPPORTED, "weight replicas need a net whose weights fit in LDS");
+    if (r > 1 && net->push_delay > 1)
+        return fail(CHAOS_EINVAL, "delayed pushes and weight replicas exclude each other");
+    if (int rc = set_device(net)) return rc;
+    if (r > net->n_replicas || (r > 1 && !net->replicas)) {
+        (void)hipFree(net->replicas);
+        (void)hipFree(net->rep_counter);
+        net->replicas = nullptr;
+        net->rep_counter = nullptr;
+        if (hipMalloc(&net->replicas, (size_t)r * net->layout.n_dev * sizeof(float)) != hipSuccess ||
+            hipMalloc(&net->rep_counter, (size_t)r * sizeof(int32_t)) != hipSuccess) {
+            (void)hipFree(net->replicas);
+            net->replicas = nullptr;
+            net->rep_counter = nullptr;
+            net->n_replicas = 1;
+            return fail(CHAOS_ENOMEM, "%d weight replicas", r);
+        }
+    }
+    net->n_replicas = r;
+    net->refresh_every = m;
     return ok();
 }
 
@@ -492,6 +528,17 @@ int chaos_train_epoch(chaos_net *net, const float *x_dev, const int32_t *labels_
     a.loss = loss_dev;
     a.claims = net->claims;
     HIP_TRY(chaos::launch_fill_i32(net->counter, 0, 2, stream), "counter reset");
+    if (kmode == chaos::kTrainAtomic && mode != CHAOS_SEQUENTIAL && net->n_replicas > 1) {
+        // every replica starts the epoch equal to the shared weights
+        a.replicas = net->replicas;
+        a.rep_counter = net->rep_counter;
+        a.n_replicas = net->n_replicas;
+        a.refresh_every = net->refresh_every;
+        HIP_TRY(chaos::launch_replicate(net->params, net->replicas, net->layout.n_dev, net->n_replicas,
+                                        stream),
+                "replica copy");
+        HIP_TRY(chaos::launch_fill_i32(net->rep_counter, 0, net->n_replicas, stream), "replica counters");
+    }
     HIP_TRY(launch(net, kmode, a, grid, stream), "train launch");
     return ok();
 }

@@ -54,6 +54,12 @@ struct WorkArgs {
     int32_t push_delay;    // training: samples between a worker's pushes (1 = per layer)
     float *stash;          // frozen weights, large net: per-sample operands of the
                            // batched conv3 / FC1 weight gradients, or null
+    float *replicas;       // atomic training, small net: [n_replicas][device floats]
+                           // copies of the weights the workers read, or null
+    int32_t *rep_counter;  // [n_replicas] samples completed per replica
+    int32_t n_replicas;    // worker b reads replica b % n_replicas
+    int32_t refresh_every; // a replica is copied from the shared weights after
+                           // every refresh_every-th sample completed on it
 };
 
 // Device layout of a net's shared weights, as segments of the canonical
@@ -86,6 +92,8 @@ hipError_t launch_axpy_mapped(float *w_dev, const float *g_can, float alpha, con
                               int64_t n_can, hipStream_t s);
 hipError_t launch_mean(const float *v, int64_t n, float *dst, hipStream_t s);
 hipError_t launch_count(const int32_t *src, float *dst, hipStream_t s);
+// dst[c * n + i] = src[i] for every copy c < copies
+hipError_t launch_replicate(const float *src, float *dst, int64_t n, int copies, hipStream_t s);
 // dst[0] = 1 if val[0] is not finite or val[0] > ref[0], else 0 (all device scalars)
 hipError_t launch_above(const float *val, const float *ref, float *dst, hipStream_t s);
 // Occupancy of the worker kernel: resident blocks per CU for a given block size.
@@ -125,5 +133,7 @@ hipError_t launch_fused_cpcp(int variant, int mode, const WorkArgs &a, int grid,
 int fused_cpcp_blocks_per_cu(int variant);
 // resident workers per CU of the small net's delayed-push kernel (0 for others)
 int fused_cpcp_delay_blocks_per_cu(int variant);
+// whether the variant's atomic training kernel can read weight replicas
+bool fused_cpcp_supports_replicas(int variant);
 
 } // namespace chaos

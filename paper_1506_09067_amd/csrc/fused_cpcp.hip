@@ -101,6 +101,7 @@ struct alignas(16) SmemCpcp {
     // delayed pushes: this worker's gradient sum since its last push (device layout)
     alignas(16) float gacc[DELAY ? S::NDEV : 4];
     int64_t idx;
+    int rep_refresh;  // this sample's worker refreshes its replica
 };
 
 // DELAY (training with atomic pushes, nets whose whole weight vector fits in
@@ -124,6 +125,13 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
     // (frozen weights, or the LDS copy) instead of the values returned by the
     // FC1 pushes
     constexpr bool kFc1Read = (MODE == kForwardBackward) || S::STAGE;
+    // Replicated weights (atomic training of a net copied whole into LDS):
+    // worker b reads replica b % n_replicas and pushes every update to the
+    // shared weights and to that replica, which is refreshed from the shared
+    // weights after every refresh_every-th sample completed on it.  Per-line
+    // contention at the memory side (every sample reads and adds into every
+    // line of the vector) is then spread over the replicas.
+    const bool kReplicas = (MODE == kTrainAtomic) && !DELAY && S::STAGE && a.replicas != nullptr;
 
     for (int k = threadIdx.x; k < 4 * S::KQ2; k += NT) {
         int c = k / 25, uv = k - 25 * c, u = uv / 5, v = uv - 5 * u;
@@ -191,15 +199,17 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         const int label = a.labels[idx];
         if constexpr (S::STAGE) {
             // the weights of this sample: all 16-byte loads are issued before
-            // the first LDS write (the vector starts 16-byte aligned)
+            // the first LDS write (the vector starts 16-byte aligned); from
+            // this worker's replica when the shared weights are replicated
+            const float *Wsrc = kReplicas ? a.replicas + (int64_t)(blockIdx.x % a.n_replicas) * S::NDEV : Wg;
             constexpr int N4 = S::NDEV / 4, PER = (N4 + NT - 1) / NT, TAIL = S::NDEV - 4 * N4;
             f4 wv[PER];
 #pragma unroll
             for (int q = 0; q < PER; ++q) {
                 const int t4 = tid + NT * q;
-                wv[q] = (t4 < N4) ? *(const f4 *)(Wg + 4 * t4) : f4{0.f, 0.f, 0.f, 0.f};
+                wv[q] = (t4 < N4) ? *(const f4 *)(Wsrc + 4 * t4) : f4{0.f, 0.f, 0.f, 0.f};
             }
-            const float wt = (tid < TAIL) ? Wg[4 * N4 + tid] : 0.0f;
+            const float wt = (tid < TAIL) ? Wsrc[4 * N4 + tid] : 0.0f;
             for (int i = tid; i < S::NX; i += NT) sm.x[i] = a.x[idx * S::NX + i];
 #pragma unroll
             for (int q = 0; q < PER; ++q) {
@@ -512,9 +522,16 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         push_now.part = a.grad_part ? a.grad_part + (int64_t)blockIdx.x * S::NPARAM : nullptr;
         // a layer's gradient element (each weight once per sample, by one
         // thread): pushed now, or added to the worker's sum
+        float *const rep = kReplicas ? a.replicas + (int64_t)(blockIdx.x % a.n_replicas) * S::NDEV : nullptr;
         auto push = [&](int w_off, int g_off, float g) {
-            if constexpr (DELAY) sm.gacc[w_off] += g;
-            else push_now(w_off, g_off, g);
+            if constexpr (DELAY) {
+                sm.gacc[w_off] += g;
+            } else {
+                push_now(w_off, g_off, g);
+                // the same update, rounded the same way, into this worker's replica
+                if (rep) __hip_atomic_fetch_add(rep + w_off, __fmul_rn(push_now.neg_lr, g), __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+            }
         };
 
         if (tid < 64) {
@@ -1037,6 +1054,26 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             }
         }
         if (kTrain && tid == 0) atomicAdd(a.counter + 1, 1);  // samples completed
+        if (kReplicas) {
+            // every refresh_every-th sample completed on this replica: once
+            // this worker's pushes have landed, copy the shared weights into it
+            // (relaxed agent-scope stores, performed where the pushes are; a
+            // concurrent push to the replica that the copy overwrites is in the
+            // shared weights and returns with the next copy)
+            if (tid == 0) {
+                const int r = blockIdx.x % a.n_replicas;
+                sm.rep_refresh = (atomicAdd(a.rep_counter + r, 1) % a.refresh_every) == a.refresh_every - 1;
+            }
+            __syncthreads();
+            if (sm.rep_refresh) {
+                wait_vector_memory();
+                __syncthreads();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+                for (int i = tid; i < S::NDEV; i += NT)
+                    __hip_atomic_store(rep + i, __hip_atomic_load(Wg + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
         __syncthreads();
     }
 }
@@ -1138,6 +1175,8 @@ int fused_cpcp_blocks_per_cu(int variant) {
     if (variant == 2) return cpcp_blocks_per_cu<Medium, kMediumMinBlocks>();
     return 0;
 }
+
+bool fused_cpcp_supports_replicas(int variant) { return variant == 1 && Small::STAGE; }
 
 int fused_cpcp_delay_blocks_per_cu(int variant) {
     if (variant != 1) return 0;

@@ -314,6 +314,15 @@ __global__ void count_kernel(const int32_t *__restrict__ src, float *__restrict_
     if (threadIdx.x == 0) dst[0] = (float)src[0];
 }
 
+// dst[c][i] = src[i] for c < copies
+__global__ void replicate_kernel(const float *__restrict__ src, float *__restrict__ dst, int64_t n,
+                                 int copies) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    const float v = src[i];
+    for (int c = 0; c < copies; ++c) dst[(int64_t)c * n + i] = v;
+}
+
 // dst[0] = 1 when *val is not finite or exceeds *ref, else 0
 __global__ void above_kernel(const float *__restrict__ val, const float *__restrict__ ref,
                              float *__restrict__ dst) {
@@ -402,6 +411,12 @@ hipError_t launch_mean(const float *v, int64_t n, float *dst, hipStream_t s) {
 
 hipError_t launch_count(const int32_t *src, float *dst, hipStream_t s) {
     count_kernel<<<1, 64, 0, s>>>(src, dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_replicate(const float *src, float *dst, int64_t n, int copies, hipStream_t s) {
+    if (n <= 0 || copies <= 0) return hipSuccess;
+    replicate_kernel<<<blocks_for(n, 256), 256, 0, s>>>(src, dst, n, copies);
     return hipGetLastError();
 }
 

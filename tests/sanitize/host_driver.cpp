@@ -21,6 +21,8 @@ hipError_t launch_axpy_mapped(float *, const float *, float, const ParamLayout &
 hipError_t launch_mean(const float *, int64_t, float *, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_count(const int32_t *, float *, hipStream_t) { return hipErrorInvalidValue; }
 hipError_t launch_above(const float *, const float *, float *, hipStream_t) { return hipErrorInvalidValue; }
+hipError_t launch_replicate(const float *, float *, int64_t, int, hipStream_t) { return hipErrorInvalidValue; }
+bool fused_cpcp_supports_replicas(int) { return false; }
 int worker_blocks_per_cu(int) { return 0; }
 bool fused_large_matches(const Net &) { return false; }
 void fused_large_layout(ParamLayout &) {}
@@ -91,6 +93,7 @@ int main() {
     CHECK(chaos_evaluate(nullptr, &f, &l, 1, nullptr, &l, nullptr) == CHAOS_EINVAL);
     CHECK(chaos_train_session(nullptr, &f, &l, 1, &f, &l, 1, 1, 1e-3f, 1.0f, 0, 0, &f, nullptr, nullptr) == CHAOS_EINVAL);
     CHECK(chaos_set_push_delay(nullptr, 2) == CHAOS_EINVAL);
+    CHECK(chaos_set_replicas(nullptr, 8, 4) == CHAOS_EINVAL);
     CHECK(chaos_set_claim_counter(nullptr, nullptr) == CHAOS_EINVAL);
     if (fails) return 1;
     std::printf("host driver ok\n");
