@@ -264,12 +264,19 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                     for (int j = 0; j < S::CT1; ++j) acc[q][j] = f4{0.f, 0.f, 0.f, 0.f};
                 }
+                // the pass's 24 inputs are read at once, ahead of the matrix
+                // instructions (selects after the scheduling barrier)
+                float xv[4][6];
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
+#pragma unroll
+                    for (int q = 0; q < 6; ++q) xv[s][q] = sm.x[base[q] + s * S::IN + lg];  // base 0 when invalid
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int s = 0; s < 4; ++s)
 #pragma unroll
                     for (int q = 0; q < 6; ++q) {
-                        const float v = sm.x[base[q] + s * S::IN + lg];  // base 0 when invalid
-                        const float av = valid[q] ? v : 0.0f;
+                        const float av = valid[q] ? xv[s][q] : 0.0f;
 #pragma unroll
                         for (int j = 0; j < S::CT1; ++j) acc[q][j] = mfma(av, bw[s][j], acc[q][j]);
                     }
@@ -690,24 +697,30 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             if (tid < S::F1) push(S::DBF1 + tid, S::OBF1 + tid, sm.dh[tid]);
         }
         __syncthreads();
-        // pool2 backward -> dense conv2 deltas; clear e1
-        for (int t = tid; t < S::C2P * 96; t += NT) {
-            int o = t / 96, p = t - 96 * o;
-            float d = 0.0f;
-            if (o < S::C2 && p < S::NY2) {
-                int py = p / S::H2, px = p - py * S::H2;
-                int q = o * S::NP2 + (py / 3) * 3 + px / 3;
-                int w = (py % 3) * 3 + px % 3;
-                if (sm.am2[q] == w) {
-                    float e;
-                    if constexpr (kFc1Read)
-                        e = (S::FC1_VEC == 4) ? sm.e2[q] + sm.e2b[q] : sm.e2[q];
-                    else
-                        e = ((sm.y2[q] + sm.y2[S::NF1 + q]) + sm.y2[2 * S::NF1 + q]) + sm.y2[3 * S::NF1 + q];
-                    d = e * dact_from_y(sm.p2[q]);
-                }
+        // pool2 backward -> dense conv2 deltas: a thread per pooled output
+        // writes its whole 3x3 window (the delta at the first maximum, zeros
+        // elsewhere; the windows tile the 9x9 map); the buffer's padding
+        // (positions 81..95 of every map, maps C2..C2P-1) is zeroed apart.
+        // Then clear e1.
+        for (int q = tid; q < S::NF1; q += NT) {
+            const int o = q / S::NP2, P = q - o * S::NP2, py = P / 3, px = P - 3 * py;
+            float e;
+            if constexpr (kFc1Read)
+                e = (S::FC1_VEC == 4) ? sm.e2[q] + sm.e2b[q] : sm.e2[q];
+            else
+                e = ((sm.y2[q] + sm.y2[S::NF1 + q]) + sm.y2[2 * S::NF1 + q]) + sm.y2[3 * S::NF1 + q];
+            const float d = e * dact_from_y(sm.p2[q]);
+            const int ag = sm.am2[q];
+            float *dst = sm.d2 + o * 96 + 3 * py * S::H2 + 3 * px;
+#pragma unroll
+            for (int w = 0; w < 9; ++w) dst[(w / 3) * S::H2 + w % 3] = (w == ag) ? d : 0.0f;
+        }
+        {
+            constexpr int TAIL = 96 - S::NY2, NPAD = S::C2 * TAIL + (S::C2P - S::C2) * 96;
+            for (int t = tid; t < NPAD; t += NT) {
+                const int o = t / TAIL;
+                sm.d2[(t < S::C2 * TAIL) ? o * 96 + S::NY2 + (t - o * TAIL) : S::C2 * 96 + (t - S::C2 * TAIL)] = 0.0f;
             }
-            sm.d2[t] = d;
         }
         for (int t = tid; t < S::C1 * S::NP1; t += NT) sm.e1[t] = 0.0f;
         __syncthreads();
@@ -724,39 +737,46 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
-            float aA[2], aB[2];
-            auto load_a = [&](float (&av)[2], int ks) {
+            // a step's weights and deltas are read a step ahead (unconditional
+            // reads from clamped addresses, zeroed by selects after the
+            // scheduling barrier, so the matrix instructions wait for their
+            // own step's reads alone)
+            float aA[2], aB[2], bA[RT2], bB[RT2];
+            auto load = [&](float (&av)[2], float (&bv)[RT2], int ks) {
                 const int o = 4 * ks + lg;
                 const float *w2 = W2 + (o < S::C2 ? o : 0) * S::W2S + c * 25;
 #pragma unroll
                 for (int t = 0; t < 2; ++t) {
                     const int uv = 16 * t + lr;
-                    const float v = w2[uv < 25 ? uv : 0];
-                    av[t] = (o < S::C2 && uv < 25) ? v : 0.0f;
+                    av[t] = w2[uv < 25 ? uv : 0];
                 }
-            };
-            auto compute = [&](const float (&av)[2], int ks) {
-                const int o = 4 * ks + lg;
-                float bv[RT2];
 #pragma unroll
-                for (int j = 0; j < RT2; ++j) {
-                    const float v = sm.d2[o * 96 + 16 * j + lr];  // o < C2P: in the buffer
-                    bv[j] = (o < S::C2) ? v : 0.0f;
-                }
+                for (int j = 0; j < RT2; ++j) bv[j] = sm.d2[o * 96 + 16 * j + lr];  // o < C2P: in the buffer
+            };
+            auto compute = [&](const float (&av)[2], const float (&bv)[RT2], int ks) {
+                __builtin_amdgcn_sched_barrier(0);
+                const int o = 4 * ks + lg;
+                float a[2], b[RT2];
+#pragma unroll
+                for (int t = 0; t < 2; ++t) a[t] = (o < S::C2 && 16 * t + lr < 25) ? av[t] : 0.0f;
+#pragma unroll
+                for (int j = 0; j < RT2; ++j) b[j] = (o < S::C2) ? bv[j] : 0.0f;
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
-                    for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
+                    for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(a[t], b[j], acc[t][j]);
             };
-            load_a(aA, 0);
+            load(aA, bA, 0);
+#pragma unroll
             for (int ks = 0; ks < S::OKS; ks += 2) {
-                if (ks + 1 < S::OKS) load_a(aB, ks + 1);
-                compute(aA, ks);
+                if (ks + 1 < S::OKS) load(aB, bB, ks + 1);
+                compute(aA, bA, ks);
                 if (ks + 1 < S::OKS) {
-                    if (ks + 2 < S::OKS) load_a(aA, ks + 2);
-                    compute(aB, ks + 1);
+                    if (ks + 2 < S::OKS) load(aA, bA, ks + 2);
+                    compute(aB, bB, ks + 1);
                 }
             }
+            __builtin_amdgcn_sched_barrier(0);
             float *dp[RT2];
 #pragma unroll
             for (int j = 0; j < RT2; ++j) {
@@ -807,40 +827,41 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     const int uv = 4 * (i0 + t) + (lr & 3);
                     wo[t] = (t < nt && uv < 25) ? (c0 + (lr >> 2)) * 25 + uv : -1;
                 }
-                // the next output maps' weights requested while the
-                // current ones compute
-                float aA[TI], aB[TI];
-                auto load_a = [&](float (&av)[TI], int ks) {
+                // the next output maps' weights and deltas are read while the
+                // current ones compute (selects after the scheduling barrier)
+                float aA[TI], aB[TI], bA[RT2], bB[RT2];
+                auto load = [&](float (&av)[TI], float (&bv)[RT2], int ks) {
                     const int o = 4 * ks + lg;
                     const float *w2 = W2 + (o < S::C2 ? o : 0) * S::W2S;
 #pragma unroll
-                    for (int t = 0; t < TI; ++t) {
-                        const float v = w2[wo[t] >= 0 ? wo[t] : 0];
-                        av[t] = (o < S::C2 && wo[t] >= 0) ? v : 0.0f;
-                    }
-                };
-                auto compute = [&](const float (&av)[TI], int ks) {
-                    const int o = 4 * ks + lg;
-                    float bv[RT2];
+                    for (int t = 0; t < TI; ++t) av[t] = w2[wo[t] >= 0 ? wo[t] : 0];
 #pragma unroll
-                    for (int j = 0; j < RT2; ++j) {
-                        const float v = sm.d2[o * 96 + 16 * j + lr];  // o < C2P: in the buffer
-                        bv[j] = (o < S::C2) ? v : 0.0f;
-                    }
+                    for (int j = 0; j < RT2; ++j) bv[j] = sm.d2[o * 96 + 16 * j + lr];  // o < C2P: in the buffer
+                };
+                auto compute = [&](const float (&av)[TI], const float (&bv)[RT2], int ks) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    const int o = 4 * ks + lg;
+                    float a[TI], b[RT2];
+#pragma unroll
+                    for (int t = 0; t < TI; ++t) a[t] = (o < S::C2 && wo[t] >= 0) ? av[t] : 0.0f;
+#pragma unroll
+                    for (int j = 0; j < RT2; ++j) b[j] = (o < S::C2) ? bv[j] : 0.0f;
 #pragma unroll
                     for (int t = 0; t < TI; ++t)
 #pragma unroll
-                        for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
+                        for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(a[t], b[j], acc[t][j]);
                 };
-                load_a(aA, 0);
+                load(aA, bA, 0);
+#pragma unroll
                 for (int ks = 0; ks < S::OKS; ks += 2) {
-                    if (ks + 1 < S::OKS) load_a(aB, ks + 1);
-                    compute(aA, ks);
+                    if (ks + 1 < S::OKS) load(aB, bB, ks + 1);
+                    compute(aA, bA, ks);
                     if (ks + 1 < S::OKS) {
-                        if (ks + 2 < S::OKS) load_a(aA, ks + 2);
-                        compute(aB, ks + 1);
+                        if (ks + 2 < S::OKS) load(aA, bA, ks + 2);
+                        compute(aB, bB, ks + 1);
                     }
                 }
+                __builtin_amdgcn_sched_barrier(0);
                 float *dp[RT2];
 #pragma unroll
                 for (int j = 0; j < RT2; ++j) {
@@ -862,11 +883,23 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             }
         };
 
+        // The conv2 bias gradients are collected in gb, the FC activations'
+        // buffer (free once the FC gradients are pushed), and pushed together
+        // by consecutive threads: one push instruction per bias block, as for
+        // every other block of weights (single-lane pushes to the same few
+        // lines would queue behind each other at the memory side).
+        float *gb = sm.h;  // the conv2 bias gradients
+        static_assert(S::C2 <= S::F1 + 16, "bias sums fit in the FC activations' buffer");
+
         // ---- conv2 weight gradient: G[o][k] = sum_p d2[o][p] p1col[p][k],
         //      pushed, in passes of JW column tiles of 16 k (JW * CT2
-        //      accumulators keep the matrix core busy) ----
+        //      accumulators keep the matrix core busy).  The first padding
+        //      column k = KC2 multiplies the deltas by ones: its entries are
+        //      the bias gradients, each map's deltas summed over the 81
+        //      positions. ----
         constexpr int NJT = S::KC2P / 16, JW = 4;
         static_assert(NJT % JW == 0, "whole passes");
+        static_assert(S::KC2 < S::KC2P, "a padding column holds the bias gradients");
         // input offset of output position p = 4s + lg (or -1 past the map)
         auto pb = [&](int s) {
             const int p = 4 * s + lg, py = p / S::H2, px = p - py * S::H2;
@@ -874,11 +907,12 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         };
         auto wgrad_pass = [&](const int jt0, const float (&ad)[S::CT2][21]) {
             const float *pc[JW];
-            bool kv[JW];
+            bool kv[JW], one[JW];
 #pragma unroll
             for (int b = 0; b < JW; ++b) {
                 const int k = 16 * (jt0 + b) + lr;
                 kv[b] = k < S::KC2;
+                one[b] = k == S::KC2;
                 pc[b] = sm.p1 + (kv[b] ? sm.koff2[k] : 0);
             }
             f4 acc[JW][S::CT2];
@@ -887,58 +921,66 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                 for (int i = 0; i < S::CT2; ++i) acc[b][i] = f4{0.f, 0.f, 0.f, 0.f};
             // operands: unconditional LDS reads from a clamped address,
-            // zeroed by a select (no branch between a read and its use)
-#pragma unroll
-            for (int s = 0; s < 21; ++s) {
-                float bv[JW];
+            // zeroed by a select (no branch between a read and its use); the
+            // next step's reads are issued before this step's matrix
+            // instructions, which then wait for this step's alone
+            auto load = [&](float (&bv)[JW], int s) {
                 const int q = pb(s);  // -1 past the map
 #pragma unroll
+                for (int b = 0; b < JW; ++b) bv[b] = pc[b][q >= 0 ? q : 0];
+            };
+            auto step = [&](const float (&bv)[JW], int s) {
+                __builtin_amdgcn_sched_barrier(0);
+                const bool qv = pb(s) >= 0;
+#pragma unroll
                 for (int b = 0; b < JW; ++b) {
-                    const float v = pc[b][q >= 0 ? q : 0];
-                    bv[b] = (kv[b] && q >= 0) ? v : 0.0f;
+                    const float v = qv ? (kv[b] ? bv[b] : (one[b] ? 1.0f : 0.0f)) : 0.0f;
+#pragma unroll
+                    for (int i = 0; i < S::CT2; ++i) acc[b][i] = mfma(ad[i][s], v, acc[b][i]);
                 }
+            };
+            float bA[JW], bB[JW];
+            load(bA, 0);
 #pragma unroll
-                for (int b = 0; b < JW; ++b)
-#pragma unroll
-                    for (int i = 0; i < S::CT2; ++i) acc[b][i] = mfma(ad[i][s], bv[b], acc[b][i]);
+            for (int s = 0; s < 21; s += 2) {
+                if (s + 1 < 21) load(bB, s + 1);
+                step(bA, s);
+                if (s + 1 < 21) {
+                    if (s + 2 < 21) load(bA, s + 2);
+                    step(bB, s + 1);
+                }
             }
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int b = 0; b < JW; ++b) {
-                if (!kv[b]) continue;
                 const int k = 16 * (jt0 + b) + lr;
+                if (kv[b]) {
 #pragma unroll
-                for (int i = 0; i < S::CT2; ++i)
+                    for (int i = 0; i < S::CT2; ++i)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        int o = 16 * i + 4 * lg + r;
-                        if (o < S::C2) push(S::DW2 + o * S::KC2S + k, S::OW2 + o * S::KC2 + k, acc[b][i][r]);
-                    }
+                        for (int r = 0; r < 4; ++r) {
+                            int o = 16 * i + 4 * lg + r;
+                            if (o < S::C2) push(S::DW2 + o * S::KC2S + k, S::OW2 + o * S::KC2 + k, acc[b][i][r]);
+                        }
+                } else if (one[b]) {
+#pragma unroll
+                    for (int i = 0; i < S::CT2; ++i)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            int o = 16 * i + 4 * lg + r;
+                            if (o < S::C2) gb[o] = acc[b][i][r];
+                        }
+                }
             }
         };
-        // Bias gradients are summed by wavefronts (lanes over positions, then a
-        // fixed butterfly) into gb, the FC activations' buffer (free once the
-        // FC gradients are pushed), and pushed together by consecutive
-        // threads: one push instruction per bias block, as for every other
-        // block of weights (single-lane pushes to the same few lines would
-        // queue behind each other at the memory side).
-        float *gb = sm.h;  // [0, C2) conv2 biases, [C2, C2 + C1) conv1 biases
-        static_assert(S::C2 + S::C1 <= S::F1 + 16, "bias sums fit in the FC activations' buffer");
         // this wavefront's weight-gradient passes (every jt0 = first + step * n)
-        // and the conv2 bias gradients of maps o = ofirst + ostep * n (a map's
-        // deltas summed over its 81 positions)
-        auto conv2_wgrad = [&](const int first, const int step, const int ofirst, const int ostep) {
+        auto conv2_wgrad = [&](const int first, const int step) {
             float ad[S::CT2][21];
 #pragma unroll
             for (int i = 0; i < S::CT2; ++i)
 #pragma unroll
                 for (int s = 0; s < 21; ++s) ad[i][s] = sm.d2[(16 * i + lr) * 96 + 4 * s + lg];
             for (int jt0 = first; jt0 < NJT; jt0 += step) wgrad_pass(jt0, ad);
-            for (int o = ofirst; o < S::C2; o += ostep) {
-                float g = 0.0f;
-                for (int p = lane; p < S::NY2; p += 64) g += sm.d2[o * 96 + p];
-                g = wave_sum(g);
-                if (lane == 0) gb[o] = g;
-            }
         };
         if constexpr (S::STAGE) {
             // Small net: backward data and weight gradient in one phase.  They
@@ -951,7 +993,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             static_assert(S::C1 == 5 && NJT == 2 * JW, "small net: 5 input maps, two passes");
             if (wave == 0) block4(0);
             else if (wave == 1) map1(4);
-            else conv2_wgrad(JW * (wave - 2), 2 * JW, wave - 2, 2);
+            else conv2_wgrad(JW * (wave - 2), 2 * JW);
         } else {
             if constexpr (S::C1 == 5 * NW) {
                 // five maps per wavefront: a 4-map block and one map alone
@@ -963,7 +1005,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 // wavefront w owns input maps w, w + 4, ...
                 for (int c = wave; c < S::C1; c += NW) map1(c);
             }
-            conv2_wgrad(JW * wave, NW * JW, wave, NW);
+            conv2_wgrad(JW * wave, NW * JW);
         }
         __syncthreads();
 
@@ -974,8 +1016,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         //      summed in wavefront order (through the free delta buffer).  The
         //      delta is nonzero only at each pooling window's maximum, where it
         //      is the pool1 error times f' of the pool1 value (pool1 backward,
-        //      formed as the operands are read).  Bias: the deltas summed per
-        //      map by one wavefront. ----
+        //      formed as the operands are read). ----
         {
             f4 acc[2][S::CT1];
 #pragma unroll
@@ -1006,32 +1047,50 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                 for (int t = 0; t < S::CT1; ++t) c[t] = mfma(av[t], bx, c[t]);
             };
-            // acc[0] takes positions wave, wave + 2 NW, ...; acc[1] wave + NW, ...
-            float bxA, bxB, avA[S::CT1], avB[S::CT1];
-            if (wave < S::NP1) operands(wave, bxA, avA);
-            for (int P = wave; P < S::NP1; P += 2 * NW) {
-                const bool q = P + NW < S::NP1;
-                if (q) operands(P + NW, bxB, avB);
-                compute(bxA, avA, acc[0]);
-                if (q) {
-                    if (P + 2 * NW < S::NP1) operands(P + 2 * NW, bxA, avA);
-                    compute(bxB, avB, acc[1]);
+            // acc[0] takes positions wave, wave + 2 NW, ...; acc[1] wave + NW,
+            // ...; the operands of the next four positions are read while the
+            // current four compute.  The conv1 bias gradients are summed from
+            // the same operands: per lane over its positions, then over the
+            // four lane groups and (after the barrier) the wavefronts in order.
+            float bxC[4], avC[4][S::CT1], bxN[4], avN[4][S::CT1], bsum[S::CT1];
+#pragma unroll
+            for (int t = 0; t < S::CT1; ++t) bsum[t] = 0.0f;
+            auto load4 = [&](int P0, float (&bx)[4], float (&av)[4][S::CT1]) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int P = P0 + NW * u;
+                    operands(P < S::NP1 ? P : S::NP1 - 1, bx[u], av[u]);
+                }
+            };
+            load4(wave, bxC, avC);
+            for (int P0 = wave; P0 < S::NP1; P0 += 4 * NW) {
+                load4(P0 + 4 * NW, bxN, avN);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (P0 + NW * u < S::NP1) {
+                        compute(bxC[u], avC[u], acc[u & 1]);
+#pragma unroll
+                        for (int t = 0; t < S::CT1; ++t) bsum[t] += avC[u][t];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    bxC[u] = bxN[u];
+#pragma unroll
+                    for (int t = 0; t < S::CT1; ++t) avC[u][t] = avN[u][t];
                 }
             }
-            // the conv2 biases summed in the previous phase; the conv1 biases:
-            // map o by wavefront o % NW, lanes over the pooled positions
+            // the conv2 biases summed in the previous phase
             if (tid < S::C2) push(S::DB2 + tid, S::OB2 + tid, gb[tid]);
-            for (int o = wave; o < S::C1; o += NW) {
-                float g = 0.0f;
-                for (int q = lane; q < S::NP1; q += 64)
-                    g += sm.e1[o * S::NP1 + q] * dact_from_y(sm.p1[o * S::NP1 + q]);
-                g = wave_sum(g);
-                if (lane == 0) gb[S::C2 + o] = g;
-            }
-            float *red = sm.d2;  // [wavefront][tile][lane][4]
+            float *red = sm.d2;  // [wavefront][tile][lane][4], then [wavefront][CT1 * 16] bias sums
+            float *redb = red + NW * S::CT1 * 256;
 #pragma unroll
-            for (int t = 0; t < S::CT1; ++t)
+            for (int t = 0; t < S::CT1; ++t) {
                 *(f4 *)(red + ((wave * S::CT1 + t) * 64 + lane) * 4) = acc[0][t] + acc[1][t];
+                const float b1 = bsum[t] + __shfl_xor(bsum[t], 16, 64);
+                const float b2 = b1 + __shfl_xor(b1, 32, 64);
+                if (lg == 0) redb[wave * S::CT1 * 16 + 16 * t + lr] = b2;
+            }
             __syncthreads();
             // weights and biases of conv1, consecutive in memory, one block
             for (int t = tid; t < S::C1 * 16 + S::C1; t += NT) {
@@ -1043,7 +1102,11 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     for (int w = 1; w < NW; ++w) g += red[(w * S::CT1 + tile) * 256 + e];
                     push(S::DW1 + t, S::OW1 + t, g);
                 } else {
-                    push(S::DB1 + t - S::C1 * 16, S::OB1 + t - S::C1 * 16, gb[S::C2 + t - S::C1 * 16]);
+                    const int o = t - S::C1 * 16;
+                    float g = redb[o];
+#pragma unroll
+                    for (int w = 1; w < NW; ++w) g += redb[w * S::CT1 * 16 + o];
+                    push(S::DB1 + o, S::OB1 + o, g);
                 }
             }
         }
@@ -1083,8 +1146,8 @@ using Medium = Cpcp<20, 40, 150>;
 static_assert(Small::NPARAM == 6405 && Medium::NPARAM == 76040, "Table I weight counts");
 static_assert(NW * Small::NF1 <= Small::C2 * Small::NY2 && NW * Medium::NF1 <= Medium::C2 * Medium::NY2,
               "FC1 partial sums fit in the conv2 output buffer");
-static_assert(NW * Small::CT1 * 256 <= Small::C2P * 96 && NW * Medium::CT1 * 256 <= Medium::C2P * 96,
-              "conv1 partial tiles fit in the delta buffer");
+static_assert(NW * Small::CT1 * 272 <= Small::C2P * 96 && NW * Medium::CT1 * 272 <= Medium::C2P * 96,
+              "conv1 partial tiles and bias sums fit in the delta buffer");
 
 template <class S, int MINB>
 hipError_t launch_cpcp(int mode, const WorkArgs &a, int grid, hipStream_t s) {
