@@ -79,6 +79,10 @@ struct Cpcp {
 
 constexpr int NT = 256, NW = 4;
 constexpr int RT2 = 6;  // conv2 output positions 81 -> 6 tiles of 16
+// Row stride of the conv2 delta buffer (96 positions read, 81 nonzero): 100
+// puts the 16 rows that one matrix operand read takes (lanes over rows) in
+// distinct LDS banks, where a stride of 96 folds them onto one or two.
+constexpr int D2S = 100;
 
 template <class S, bool DELAY = false>
 struct alignas(16) SmemCpcp {
@@ -86,7 +90,7 @@ struct alignas(16) SmemCpcp {
     float p1[S::C1 * S::NP1];            // pool1 output, later pool1 errors/deltas in e1
     float e1[S::C1 * S::NP1];            // dE/d(pool1 output)
     float y2[S::C2 * S::NY2];            // conv2 output before the activation
-    alignas(16) float d2[S::C2P * 96];   // conv2 output deltas (dense, zero off the argmax);
+    alignas(16) float d2[S::C2P * D2S];   // conv2 output deltas (dense, zero off the argmax);
                                          // conv2 forward partial sums before that
     alignas(16) float p2[S::NF1];        // pool2 output
     float e2[S::NF1], e2b[S::NF1];       // its errors (two partial sums over FC1 rows)
@@ -711,15 +715,15 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 e = ((sm.y2[q] + sm.y2[S::NF1 + q]) + sm.y2[2 * S::NF1 + q]) + sm.y2[3 * S::NF1 + q];
             const float d = e * dact_from_y(sm.p2[q]);
             const int ag = sm.am2[q];
-            float *dst = sm.d2 + o * 96 + 3 * py * S::H2 + 3 * px;
+            float *dst = sm.d2 + o * D2S + 3 * py * S::H2 + 3 * px;
 #pragma unroll
             for (int w = 0; w < 9; ++w) dst[(w / 3) * S::H2 + w % 3] = (w == ag) ? d : 0.0f;
         }
         {
-            constexpr int TAIL = 96 - S::NY2, NPAD = S::C2 * TAIL + (S::C2P - S::C2) * 96;
+            constexpr int TAIL = D2S - S::NY2, NPAD = S::C2 * TAIL + (S::C2P - S::C2) * D2S;
             for (int t = tid; t < NPAD; t += NT) {
                 const int o = t / TAIL;
-                sm.d2[(t < S::C2 * TAIL) ? o * 96 + S::NY2 + (t - o * TAIL) : S::C2 * 96 + (t - S::C2 * TAIL)] = 0.0f;
+                sm.d2[(t < S::C2 * TAIL) ? o * D2S + S::NY2 + (t - o * TAIL) : S::C2 * D2S + (t - S::C2 * TAIL)] = 0.0f;
             }
         }
         for (int t = tid; t < S::C1 * S::NP1; t += NT) sm.e1[t] = 0.0f;
@@ -751,7 +755,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     av[t] = w2[uv < 25 ? uv : 0];
                 }
 #pragma unroll
-                for (int j = 0; j < RT2; ++j) bv[j] = sm.d2[o * 96 + 16 * j + lr];  // o < C2P: in the buffer
+                for (int j = 0; j < RT2; ++j) bv[j] = sm.d2[o * D2S + 16 * j + lr];  // o < C2P: in the buffer
             };
             auto compute = [&](const float (&av)[2], const float (&bv)[RT2], int ks) {
                 __builtin_amdgcn_sched_barrier(0);
@@ -836,7 +840,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                     for (int t = 0; t < TI; ++t) av[t] = w2[wo[t] >= 0 ? wo[t] : 0];
 #pragma unroll
-                    for (int j = 0; j < RT2; ++j) bv[j] = sm.d2[o * 96 + 16 * j + lr];  // o < C2P: in the buffer
+                    for (int j = 0; j < RT2; ++j) bv[j] = sm.d2[o * D2S + 16 * j + lr];  // o < C2P: in the buffer
                 };
                 auto compute = [&](const float (&av)[TI], const float (&bv)[RT2], int ks) {
                     __builtin_amdgcn_sched_barrier(0);
@@ -979,7 +983,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
             for (int i = 0; i < S::CT2; ++i)
 #pragma unroll
-                for (int s = 0; s < 21; ++s) ad[i][s] = sm.d2[(16 * i + lr) * 96 + 4 * s + lg];
+                for (int s = 0; s < 21; ++s) ad[i][s] = sm.d2[(16 * i + lr) * D2S + 4 * s + lg];
             for (int jt0 = first; jt0 < NJT; jt0 += step) wgrad_pass(jt0, ad);
         };
         if constexpr (S::STAGE) {
@@ -1146,7 +1150,7 @@ using Medium = Cpcp<20, 40, 150>;
 static_assert(Small::NPARAM == 6405 && Medium::NPARAM == 76040, "Table I weight counts");
 static_assert(NW * Small::NF1 <= Small::C2 * Small::NY2 && NW * Medium::NF1 <= Medium::C2 * Medium::NY2,
               "FC1 partial sums fit in the conv2 output buffer");
-static_assert(NW * Small::CT1 * 272 <= Small::C2P * 96 && NW * Medium::CT1 * 272 <= Medium::C2P * 96,
+static_assert(NW * Small::CT1 * 272 <= Small::C2P * D2S && NW * Medium::CT1 * 272 <= Medium::C2P * D2S,
               "conv1 partial tiles and bias sums fit in the delta buffer");
 
 template <class S, int MINB>
