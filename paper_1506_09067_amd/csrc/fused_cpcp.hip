@@ -72,6 +72,14 @@ struct Cpcp {
     static constexpr bool STAGE2 = !STAGE && NW2 <= 20480 && DW2 % 4 == 0 && KC2 % 4 == 0;
     // row stride of the conv2 weights as the kernel reads them
     static constexpr int W2S = STAGE2 ? KC2 : KC2S;
+    // Such a net copies its small segments into LDS with them: the conv1
+    // weights and biases [DW1, DB1 + C1), the conv2 biases, and everything
+    // from the FC1 biases on (the FC2 weights and biases), so that no read of
+    // the sample but the FC1 rows goes to memory.
+    static constexpr int NLO = DB1 + C1, NTAIL = NDEV - DBF1;
+    static constexpr int NSMALL = STAGE2 ? NLO + C2 + NTAIL : 4;
+    static_assert(!STAGE2 || (DW1 == 0 && NLO % 4 == 0 && DB2 % 4 == 0 && C2 % 4 == 0 && DBF1 % 4 == 0),
+                  "the small segments are copied with 16-byte loads");
     // 16-byte loads of conv2 weight rows need 16-byte aligned row starts (the
     // LDS copies are 16-byte aligned; a row's padding reads as zero)
     static constexpr bool W2_ALIGNED16 = ((STAGE2 ? 0 : DW2) % 4 == 0) && (W2S % 4 == 0);
@@ -101,6 +109,7 @@ struct alignas(16) SmemCpcp {
     unsigned char am2[S::NF1 + 16];
     alignas(16) float w[S::STAGE ? S::NDEV : 4];  // the weights read at the start of the sample
     alignas(16) float w2[S::STAGE2 ? S::NW2 : 4];    // the conv2 weights read at the start of the sample
+    alignas(16) float ws[S::NSMALL];                 // and the small segments (STAGE2)
     float sink[64];                      // scatter target of padding lanes
     // delayed pushes: this worker's gradient sum since its last push (device layout)
     alignas(16) float gacc[DELAY ? S::NDEV : 4];
@@ -124,6 +133,9 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
     // every weight read below goes through W: the LDS copy or the shared vector
     const float *W = S::STAGE ? (const float *)sm.w : Wg;
     const float *W2 = S::STAGE2 ? (const float *)sm.w2 : W + S::DW2;  // conv2 weights [o][k], rows W2S apart
+    const float *Wlo = S::STAGE2 ? (const float *)sm.ws : W;                      // conv1 weights and biases
+    const float *Wb2 = S::STAGE2 ? (const float *)sm.ws + S::NLO : W + S::DB2;   // conv2 biases
+    const float *Wt = S::STAGE2 ? (const float *)sm.ws + S::NLO + S::C2 : W + S::DBF1;  // from the FC1 biases on
     constexpr bool kTrain = (MODE == kTrainAtomic || MODE == kTrainRacy);
     // the FC1 partial derivatives come from a separate read of the weights
     // (frozen weights, or the LDS copy) instead of the values returned by the
@@ -231,11 +243,27 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 const int o = 4 * t4 / S::KC2, k = 4 * t4 - o * S::KC2;  // a row holds whole 16-byte groups
                 wv[q] = (t4 < N4) ? *(const f4 *)(Wg + S::DW2 + o * S::KC2S + k) : f4{0.f, 0.f, 0.f, 0.f};
             }
+            constexpr int N4L = S::NLO / 4, N4B = S::C2 / 4, N4S = (S::NLO + S::C2 + S::NTAIL) / 4;
+            constexpr int PS = (N4S + NT - 1) / NT;
+            f4 sv[PS];
+#pragma unroll
+            for (int q = 0; q < PS; ++q) {
+                const int t4 = tid + NT * q;
+                const float *src = (t4 < N4L) ? Wg + 4 * t4
+                                   : (t4 < N4L + N4B) ? Wg + S::DB2 + 4 * (t4 - N4L)
+                                                      : Wg + S::DBF1 + 4 * (t4 - N4L - N4B);
+                sv[q] = (t4 < N4S) ? *(const f4 *)src : f4{0.f, 0.f, 0.f, 0.f};
+            }
             for (int i = tid; i < S::NX; i += NT) sm.x[i] = a.x[idx * S::NX + i];
 #pragma unroll
             for (int q = 0; q < PER; ++q) {
                 const int t4 = tid + NT * q;
                 if (t4 < N4) *(f4 *)(sm.w2 + 4 * t4) = wv[q];
+            }
+#pragma unroll
+            for (int q = 0; q < PS; ++q) {
+                const int t4 = tid + NT * q;
+                if (t4 < N4S) *(f4 *)(sm.ws + 4 * t4) = sv[q];
             }
         } else {
             for (int i = tid; i < S::NX; i += NT) sm.x[i] = a.x[idx * S::NX + i];
@@ -250,11 +278,11 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                 for (int j = 0; j < S::CT1; ++j) {
                     int o = 16 * j + lr;
-                    bw[s][j] = (o < S::C1) ? W[S::DW1 + o * 16 + 4 * s + lg] : 0.0f;
+                    bw[s][j] = (o < S::C1) ? Wlo[S::DW1 + o * 16 + 4 * s + lg] : 0.0f;
                 }
             float b1[S::CT1];
 #pragma unroll
-            for (int j = 0; j < S::CT1; ++j) b1[j] = (16 * j + lr < S::C1) ? W[S::DB1 + 16 * j + lr] : 0.0f;
+            for (int j = 0; j < S::CT1; ++j) b1[j] = (16 * j + lr < S::C1) ? Wlo[S::DB1 + 16 * j + lr] : 0.0f;
             // a wavefront's tiles i = wave + 4q, six at a time
             for (int i0 = wave; i0 < 43; i0 += 6 * NW) {
                 f4 acc[6][S::CT1];
@@ -399,7 +427,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 for (int j = 0; j < S::CT2; ++j) {
                     int o = 16 * j + lr;
                     if (o >= S::C2) continue;
-                    float bias = W[S::DB2 + o];
+                    float bias = Wb2[o];
 #pragma unroll
                     for (int i = 0; i < 3; ++i) {
                         f4 t = acc[i][j] + *(const f4 *)(red + ((i * S::CT2 + j) * 64 + lane) * 4);
@@ -496,7 +524,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 t1 += __shfl_xor(t1, 2, 64);
                 t1 += __shfl_xor(t1, 1, 64);
                 const int j = j0 + ((lane >> 3) & 7);
-                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[S::DBF1 + j]);
+                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + Wt[j]);
             }
         }
         __syncthreads();
@@ -505,10 +533,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
             for (int it = 0; it < (S::F1 + 63) / 64; ++it) {
                 int i = lane + 64 * it;
-                if (i < S::F1) s = fmaf(W[S::DF2 + j * S::F1S + i], sm.h[i], s);
+                if (i < S::F1) s = fmaf(Wt[S::DF2 - S::DBF1 + j * S::F1S + i], sm.h[i], s);
             }
             s = wave_sum(s);
-            if (lane == 0) sm.o[j] = act_y(s + W[S::DBF2 + j]);
+            if (lane == 0) sm.o[j] = act_y(s + Wt[S::DBF2 - S::DBF1 + j]);
         }
         __syncthreads();
         if (a.out && tid < S::F2) a.out[idx * S::F2 + tid] = sm.o[tid];
@@ -561,7 +589,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         for (int i = tid; i < S::F1; i += NT) {
             float wv[S::F2];
 #pragma unroll
-            for (int j = 0; j < S::F2; ++j) wv[j] = W[S::DF2 + j * S::F1S + i];
+            for (int j = 0; j < S::F2; ++j) wv[j] = Wt[S::DF2 - S::DBF1 + j * S::F1S + i];
             float s = 0.0f;
 #pragma unroll
             for (int j = 0; j < S::F2; ++j) s = fmaf(wv[j], sm.dout[j], s);
