@@ -111,6 +111,7 @@ struct alignas(16) SmemCpcp {
     alignas(16) float w2[S::STAGE2 ? S::NW2 : 4];    // the conv2 weights read at the start of the sample
     alignas(16) float ws[S::NSMALL];                 // and the small segments (STAGE2)
     float sink[64];                      // scatter target of padding lanes
+    float ones[128];                     // the conv2 weight gradient's ones column (bias)
     // delayed pushes: this worker's gradient sum since its last push (device layout)
     alignas(16) float gacc[DELAY ? S::NDEV : 4];
     int64_t idx;
@@ -149,6 +150,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
     // line of the vector) is then spread over the replicas.
     const bool kReplicas = (MODE == kTrainAtomic) && !DELAY && S::STAGE && a.replicas != nullptr;
 
+    for (int k = threadIdx.x; k < 128; k += NT) sm.ones[k] = 1.0f;
     for (int k = threadIdx.x; k < 4 * S::KQ2; k += NT) {
         int c = k / 25, uv = k - 25 * c, u = uv / 5, v = uv - 5 * u;
         sm.koff2[k] = (k < S::KC2) ? c * S::NP1 + u * S::Q1 + v : 0;
@@ -308,9 +310,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 for (int s = 0; s < 4; ++s)
 #pragma unroll
                     for (int q = 0; q < 6; ++q) {
-                        const float av = valid[q] ? xv[s][q] : 0.0f;
+                        // (a row past the map reads a valid input; its output
+                        // row is never used)
 #pragma unroll
-                        for (int j = 0; j < S::CT1; ++j) acc[q][j] = mfma(av, bw[s][j], acc[q][j]);
+                        for (int j = 0; j < S::CT1; ++j) acc[q][j] = mfma(xv[s][q], bw[s][j], acc[q][j]);
                     }
 #pragma unroll
                 for (int q = 0; q < 6; ++q) {
@@ -392,10 +395,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 for (int e = 0; e < 4; ++e) {
 #pragma unroll
                     for (int i = 0; i < 3; ++i) {
-                        const float v = sm.p1[base[i] + offs[e]];  // base 0 when invalid
-                        const float av = pv[i] ? v : 0.0f;
+                        // base 0 past the map: a valid input, in an output row never used
+                        const float v = sm.p1[base[i] + offs[e]];
 #pragma unroll
-                        for (int j = 0; j < S::CT2; ++j) acc[i][j] = mfma(av, b[j][e], acc[i][j]);
+                        for (int j = 0; j < S::CT2; ++j) acc[i][j] = mfma(v, b[j][e], acc[i][j]);
                     }
                 }
             };
@@ -769,10 +772,11 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int j = 0; j < RT2; ++j) acc[t][j] = f4{0.f, 0.f, 0.f, 0.f};
-            // a step's weights and deltas are read a step ahead (unconditional
-            // reads from clamped addresses, zeroed by selects after the
-            // scheduling barrier, so the matrix instructions wait for their
-            // own step's reads alone)
+            // a step's weights and deltas are read a step ahead, from clamped
+            // addresses (the matrix instructions, behind a scheduling barrier,
+            // wait for their own step's reads alone).  No operand needs
+            // zeroing: a weight row past 25 feeds an output row never
+            // scattered, and the deltas of maps C2..C2P-1 are zero.
             float aA[2], aB[2], bA[RT2], bB[RT2];
             auto load = [&](float (&av)[2], float (&bv)[RT2], int ks) {
                 const int o = 4 * ks + lg;
@@ -785,27 +789,21 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                 for (int j = 0; j < RT2; ++j) bv[j] = sm.d2[o * D2S + 16 * j + lr];  // o < C2P: in the buffer
             };
-            auto compute = [&](const float (&av)[2], const float (&bv)[RT2], int ks) {
+            auto compute = [&](const float (&av)[2], const float (&bv)[RT2]) {
                 __builtin_amdgcn_sched_barrier(0);
-                const int o = 4 * ks + lg;
-                float a[2], b[RT2];
-#pragma unroll
-                for (int t = 0; t < 2; ++t) a[t] = (o < S::C2 && 16 * t + lr < 25) ? av[t] : 0.0f;
-#pragma unroll
-                for (int j = 0; j < RT2; ++j) b[j] = (o < S::C2) ? bv[j] : 0.0f;
 #pragma unroll
                 for (int t = 0; t < 2; ++t)
 #pragma unroll
-                    for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(a[t], b[j], acc[t][j]);
+                    for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
             };
             load(aA, bA, 0);
 #pragma unroll
             for (int ks = 0; ks < S::OKS; ks += 2) {
                 if (ks + 1 < S::OKS) load(aB, bB, ks + 1);
-                compute(aA, bA, ks);
+                compute(aA, bA);
                 if (ks + 1 < S::OKS) {
                     if (ks + 2 < S::OKS) load(aA, bA, ks + 2);
-                    compute(aB, bB, ks + 1);
+                    compute(aB, bB);
                 }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -860,7 +858,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     wo[t] = (t < nt && uv < 25) ? (c0 + (lr >> 2)) * 25 + uv : -1;
                 }
                 // the next output maps' weights and deltas are read while the
-                // current ones compute (selects after the scheduling barrier)
+                // current ones compute (as in map1: no operand needs zeroing)
                 float aA[TI], aB[TI], bA[RT2], bB[RT2];
                 auto load = [&](float (&av)[TI], float (&bv)[RT2], int ks) {
                     const int o = 4 * ks + lg;
@@ -870,27 +868,21 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
 #pragma unroll
                     for (int j = 0; j < RT2; ++j) bv[j] = sm.d2[o * D2S + 16 * j + lr];  // o < C2P: in the buffer
                 };
-                auto compute = [&](const float (&av)[TI], const float (&bv)[RT2], int ks) {
+                auto compute = [&](const float (&av)[TI], const float (&bv)[RT2]) {
                     __builtin_amdgcn_sched_barrier(0);
-                    const int o = 4 * ks + lg;
-                    float a[TI], b[RT2];
-#pragma unroll
-                    for (int t = 0; t < TI; ++t) a[t] = (o < S::C2 && wo[t] >= 0) ? av[t] : 0.0f;
-#pragma unroll
-                    for (int j = 0; j < RT2; ++j) b[j] = (o < S::C2) ? bv[j] : 0.0f;
 #pragma unroll
                     for (int t = 0; t < TI; ++t)
 #pragma unroll
-                        for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(a[t], b[j], acc[t][j]);
+                        for (int j = 0; j < RT2; ++j) acc[t][j] = mfma(av[t], bv[j], acc[t][j]);
                 };
                 load(aA, bA, 0);
 #pragma unroll
                 for (int ks = 0; ks < S::OKS; ks += 2) {
                     if (ks + 1 < S::OKS) load(aB, bB, ks + 1);
-                    compute(aA, bA, ks);
+                    compute(aA, bA);
                     if (ks + 1 < S::OKS) {
                         if (ks + 2 < S::OKS) load(aA, bA, ks + 2);
-                        compute(aB, bB, ks + 1);
+                        compute(aB, bB);
                     }
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -945,17 +937,20 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 const int k = 16 * (jt0 + b) + lr;
                 kv[b] = k < S::KC2;
                 one[b] = k == S::KC2;
-                pc[b] = sm.p1 + (kv[b] ? sm.koff2[k] : 0);
+                // the ones column reads ones; the other padding columns read
+                // valid inputs into outputs never pushed
+                pc[b] = one[b] ? (const float *)sm.ones : sm.p1 + (kv[b] ? sm.koff2[k] : 0);
             }
             f4 acc[JW][S::CT2];
 #pragma unroll
             for (int b = 0; b < JW; ++b)
 #pragma unroll
                 for (int i = 0; i < S::CT2; ++i) acc[b][i] = f4{0.f, 0.f, 0.f, 0.f};
-            // operands: unconditional LDS reads from a clamped address,
-            // zeroed by a select (no branch between a read and its use); the
-            // next step's reads are issued before this step's matrix
-            // instructions, which then wait for this step's alone
+            // operands: LDS reads from a clamped address (a position past the
+            // map reads a valid input, and its deltas, the A operand, are the
+            // zeros of the delta rows' padding); the next step's reads are
+            // issued before this step's matrix instructions, which then wait
+            // for this step's alone
             auto load = [&](float (&bv)[JW], int s) {
                 const int q = pb(s);  // -1 past the map
 #pragma unroll
@@ -963,13 +958,10 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
             };
             auto step = [&](const float (&bv)[JW], int s) {
                 __builtin_amdgcn_sched_barrier(0);
-                const bool qv = pb(s) >= 0;
 #pragma unroll
-                for (int b = 0; b < JW; ++b) {
-                    const float v = qv ? (kv[b] ? bv[b] : (one[b] ? 1.0f : 0.0f)) : 0.0f;
+                for (int b = 0; b < JW; ++b)
 #pragma unroll
-                    for (int i = 0; i < S::CT2; ++i) acc[b][i] = mfma(ad[i][s], v, acc[b][i]);
-                }
+                    for (int i = 0; i < S::CT2; ++i) acc[b][i] = mfma(ad[i][s], bv[b], acc[b][i]);
             };
             float bA[JW], bB[JW];
             load(bA, 0);

@@ -64,6 +64,12 @@ static_assert(KC2S == KC2P && KC3 % 16 == 0, "16-byte weight loads stay inside o
 constexpr int NT = 256;   // threads per worker
 constexpr int NW = NT / 64;
 constexpr int FC1_ROWS = 4;  // FC1 rows a wavefront pushes per step (returning adds)
+// conv2 weight-gradient column tiles of wavefront 0 (which also takes the
+// fifth backward-data block) and of wavefronts 1 and 2 (wavefront 3 takes the
+// rest of the 32)
+constexpr int kT1W0 = 3, kT1W = 10;
+// pooled positions whose operands the weight gradient reads at once
+constexpr int kT1Pos = 6;
 
 // conv3 output rows m = 4 * P + w (P pooled 3x3 position, w window element)
 constexpr int M3 = 36, M3P = 48;                // padded to 3 tiles of 16
@@ -861,19 +867,20 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
             }
         };
         // Weight gradient G[o][k] = sum_m d2[o][m] a1col[m][k], pushed: rows o
-        // (4 tiles), four column tiles of k = (c,u,v) per pass, K = the 484
-        // outputs in (P, w) order, one pooled position per k-step;
-        // d2[o][(P, w)] is the pooled delta where w is the window's maximum
-        // and 0 elsewhere.
-        auto wgrad_tiles = [&](int jt0, int nt) {
-            f4 acc[4][4];
+        // (4 tiles), NTT column tiles of k = (c,u,v) per pass (NTT fixed at
+        // compile time: a pass computes no padding tile), K = the 484 outputs
+        // in (P, w) order, one pooled position per k-step; d2[o][(P, w)] is
+        // the pooled delta where w is the window's maximum and 0 elsewhere.
+        auto wgrad_tiles = [&](int jt0, auto ntt_c) {
+            constexpr int NTT = decltype(ntt_c)::value;
+            f4 acc[4][NTT];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int q = 0; q < 4; ++q) acc[i][q] = f4{0.f, 0.f, 0.f, 0.f};
-            int ko[4];
+                for (int q = 0; q < NTT; ++q) acc[i][q] = f4{0.f, 0.f, 0.f, 0.f};
+            int ko[NTT];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) ko[q] = (q < nt) ? sm.koff2[16 * (jt0 + q) + lr] : 0;
+            for (int q = 0; q < NTT; ++q) ko[q] = sm.koff2[16 * (jt0 + q) + lr];
             int orow[4];
             bool ovv[4];
 #pragma unroll
@@ -882,11 +889,9 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 orow[i] = (ovv[i] ? 16 * i + lr : 0) * NY2;
             }
             const int wy = lg >> 1, wx = lg & 1;
-            // operands of pooled position P (read one position ahead)
-            // raw reads here, the selects in compute behind a scheduling
-            // barrier: the next position's reads are issued before this
-            // position's matrix instructions wait for anything
-            auto operands = [&](int P, int (&am)[4], float (&av)[4], float (&bv)[4]) {
+            // operands of pooled position P: raw reads, the selects in
+            // compute behind a scheduling barrier
+            auto operands = [&](int P, int (&am)[4], float (&av)[4], float (&bv)[NTT]) {
                 const int py = P / Q2, px = P - py * Q2;
                 const int base = (2 * py + wy) * H1 + 2 * px + wx;
 #pragma unroll
@@ -895,32 +900,35 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     av[i] = sm.y2[orow[i] + P];
                 }
 #pragma unroll
-                for (int q = 0; q < 4; ++q) bv[q] = sm.a1[base + ko[q]];
+                for (int q = 0; q < NTT; ++q) bv[q] = sm.a1[base + ko[q]];
             };
-            auto compute = [&](const int (&am)[4], const float (&av)[4], const float (&bv)[4]) {
-                __builtin_amdgcn_sched_barrier(0);
+            auto compute = [&](const int (&am)[4], const float (&av)[4], const float (&bv)[NTT]) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const float a = (ovv[i] && am[i] == lg) ? av[i] : 0.0f;
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) acc[i][q] = mfma(a, bv[q], acc[i][q]);
+                    for (int q = 0; q < NTT; ++q) acc[i][q] = mfma(a, bv[q], acc[i][q]);
                 }
             };
-            int mA[4], mB[4];
-            float aA[4], bA[4], aB[4], bB[4];
-            operands(0, mA, aA, bA);
-            for (int P = 0; P < NY2; P += 2) {
-                if (P + 1 < NY2) operands(P + 1, mB, aB, bB);
-                compute(mA, aA, bA);
-                if (P + 1 < NY2) {
-                    if (P + 2 < NY2) operands(P + 2, mA, aA, bA);
-                    compute(mB, aB, bB);
-                }
-            }
+            // KPOS positions per iteration: all their reads first, then their
+            // matrix instructions in position order, each waiting for its own
+            // position's reads (no read crosses the loop's back edge, where
+            // the register allocator's copies would wait for all of them)
+            for (int P0 = 0; P0 < NY2; P0 += kT1Pos) {
+                int am[kT1Pos][4];
+                float av[kT1Pos][4], bv[kT1Pos][NTT];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
+                for (int u = 0; u < kT1Pos; ++u) operands(P0 + u < NY2 ? P0 + u : NY2 - 1, am[u], av[u], bv[u]);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int u = 0; u < kT1Pos; ++u)
+                    if (P0 + u < NY2) compute(am[u], av[u], bv[u]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int q = 0; q < NTT; ++q) {
                 const int k = 16 * (jt0 + q) + lr;
-                if (q >= nt || k >= KC2) continue;
+                if (k >= KC2) continue;
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -930,13 +938,22 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     }
             }
         };
+        // this wavefront's column tiles [t0, t1): passes of four, then one of
+        // the remainder
+        auto wgrad_range = [&](int t0, int t1) {
+            int jt = t0;
+            for (; jt + 4 <= t1; jt += 4) wgrad_tiles(jt, std::integral_constant<int, 4>{});
+            if (t1 - jt == 3) wgrad_tiles(jt, std::integral_constant<int, 3>{});
+            else if (t1 - jt == 2) wgrad_tiles(jt, std::integral_constant<int, 2>{});
+            else if (t1 - jt == 1) wgrad_tiles(jt, std::integral_constant<int, 1>{});
+        };
         {
             bwd_block(wave);
             if (wave == 0) bwd_block(4);
             // column tiles [t0, t1) of this wavefront
-            const int t0 = (wave == 0) ? 0 : 3 + 10 * (wave - 1);
-            const int t1 = (wave == 0) ? 3 : (wave == 3 ? 32 : t0 + 10);
-            for (int jt = t0; jt < t1; jt += 4) wgrad_tiles(jt, (t1 - jt < 4) ? t1 - jt : 4);
+            const int t0 = (wave == 0) ? 0 : kT1W0 + kT1W * (wave - 1);
+            const int t1 = (wave == 0) ? kT1W0 : (wave == 3 ? 32 : t0 + kT1W);
+            wgrad_range(t0, t1);
             if (tid < C2) {
                 float g4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 4
