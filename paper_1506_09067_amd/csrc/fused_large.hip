@@ -82,7 +82,7 @@ struct alignas(16) Smem {
     union {
         struct {
             float s2[C2 * NY2];          // conv3 backward-data sums, then pool1 errors
-            float d3[C3 * M3P];          // conv3 output deltas, rows (P, w)
+            alignas(16) float d3[C3 * M3P];  // conv3 output deltas, rows (P, w)
         };
         float red3[2 * 21 * 256];        // conv3 split-K partial sums (forward only)
         float w2s[KC2 * 65];             // conv2 weights staged as [k][o] (forward only)
@@ -97,6 +97,7 @@ struct alignas(16) Smem {
     unsigned char am1[C1 * NP1 + 12];    // pool1 argmax (window element 0..3)
     unsigned char am3[NF1 + 4];          // pool2 argmax
     float sink[128];                     // scatter target of padding lanes
+    float zero[4];                       // a zero operand for K padding (set once)
     int64_t idx;
 };
 static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
@@ -118,6 +119,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         sm.koff2[k] = (k < KC2) ? c * NP1 + u * Q1 + v : 0;
     }
 
+    if (threadIdx.x < 4) sm.zero[threadIdx.x] = 0.0f;
     for (int64_t step = 0;; ++step) {
         // The thread index is made opaque to the optimizer at the top of each
         // sample: index arithmetic of every phase then stays inside its phase
@@ -207,7 +209,8 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 for (int s = 0; s < 4; ++s)
 #pragma unroll
                     for (int q = 0; q < 6; ++q) {
-                        float av = valid[q] ? sm.x[base[q] + s * IN + lg] : 0.0f;
+                        // (base 0 past the map: a valid input, in an output row never used)
+                        const float av = sm.x[base[q] + s * IN + lg];
                         acc[q][0] = mfma(av, bw[s][0], acc[q][0]);
                         acc[q][1] = mfma(av, bw[s][1], acc[q][1]);
                     }
@@ -638,14 +641,20 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 sm.e3[q] = ((part[q] + part[NF1 + q]) + part[2 * NF1 + q]) + part[3 * NF1 + q];
             __syncthreads();
         }
-        for (int t = tid; t < C3 * M3P; t += NT) {
-            int o = t / M3P, m = t - o * M3P;
-            float d = 0.0f;
-            if (m < M3) {
-                int P = m >> 2, w = m & 3, q = o * NP3 + P;
-                if (sm.am3[q] == w) d = sm.e3[q] * dact_from_y(sm.p3[q]);
-            }
-            sm.d3[t] = d;
+        // (a thread per pooled output writes its window's four deltas, rows
+        // 4P..4P+3 of its map, as one 16-byte store: the delta at the first
+        // maximum, zeros elsewhere; rows M3..M3P-1 of every map are zeroed apart)
+#pragma unroll 1
+        for (int q = tid; q < NF1; q += NT) {
+            const int o = q / NP3, P = q - o * NP3, ag = sm.am3[q];
+            const float d = sm.e3[q] * dact_from_y(sm.p3[q]);
+            *(f4 *)(sm.d3 + o * M3P + 4 * P) = f4{ag == 0 ? d : 0.0f, ag == 1 ? d : 0.0f, ag == 2 ? d : 0.0f,
+                                                  ag == 3 ? d : 0.0f};
+        }
+        static_assert(M3 % 4 == 0 && M3P % 4 == 0, "16-byte delta rows");
+        for (int t = tid; t < C3 * (M3P - M3) / 4; t += NT) {
+            const int o = t / ((M3P - M3) / 4), r = t - o * ((M3P - M3) / 4);
+            *(f4 *)(sm.d3 + o * M3P + M3 + 4 * r) = f4{0.f, 0.f, 0.f, 0.f};
         }
         for (int t = tid; t < C2 * NY2; t += NT) sm.s2[t] = 0.0f;
         __syncthreads();
@@ -938,29 +947,29 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 kval[j] = k < KC2;
                 boff[j] = kval[j] ? sm.koff2[k] : 0;
             }
-            // operands: unconditional LDS reads from clamped addresses (a
-            // select zeroes the padding), the next step's read while this
-            // step's matrix instructions run
+            // operands: LDS reads from clamped addresses, the next step's
+            // reads while this step's matrix instructions run.  Nothing is
+            // zeroed between the matrix instructions: rows past C2 and columns
+            // past KC2 only feed outputs never pushed, and a k-step position
+            // past the 121 outputs (K padding) reads its deltas from a zero.
             auto load = [&](float (&av)[4], float (&bv)[3], int ks) {
                 const int p = 4 * ks + lg, pc = p < NY2 ? p : 0;
                 const int py = pc / H2, px = pc - py * H2, pb = py * Q1 + px;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int o = 16 * i + lr;
-                    av[i] = sm.y2[(o < C2 ? o : 0) * NY2 + pc];
+                    const float *src = (p < NY2) ? sm.y2 + (o < C2 ? o : 0) * NY2 + p : sm.zero;
+                    av[i] = *src;
                 }
 #pragma unroll
                 for (int j = 0; j < 3; ++j) bv[j] = sm.p1[boff[j] + pb];  // boff 0 when invalid
             };
-            auto step = [&](const float (&av)[4], const float (&bv)[3], int ks) {
-                const bool pv = 4 * ks + lg < NY2;
+            auto step = [&](const float (&av)[4], const float (&bv)[3], int) {
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float a = (pv && 16 * i + lr < C2) ? av[i] : 0.0f;
+                for (int i = 0; i < 4; ++i)
 #pragma unroll
-                    for (int j = 0; j < 3; ++j) acc[i][j] = mfma(a, kval[j] ? bv[j] : 0.0f, acc[i][j]);
-                }
+                    for (int j = 0; j < 3; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
             };
             float aA[4], bA[3], aB[4], bB[3];
             load(aA, bA, 0);
@@ -999,7 +1008,7 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         // the input under the kernel, as a GEMM on the matrix cores: rows o
         // (2 tiles), cols uv = 4u + v, K = 4P + w with the pooled positions
         // P split over the wavefronts; the four partial tiles are summed in
-        // wavefront order.  Bias gradient: the deltas summed per map.
+        // wavefront order.
         {
             f4 acc[2][2];
 #pragma unroll
@@ -1009,27 +1018,47 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
             const int oa = lr, ob = (16 + lr < C1) ? 16 + lr : 0;
             const bool vb = 16 + lr < C1;
             const int xo = ((lg >> 1) + (lr >> 2)) * IN + (lg & 1) + (lr & 3);
-            auto step = [&](int P, f4 (&c)[2]) {
-                const int py = P / Q1, px = P - py * Q1;
-                const float bx = sm.x[2 * py * IN + 2 * px + xo];
-                // both reads unconditional (ob is 0 when the map is past C1)
-                const int m0 = sm.am1[oa * NP1 + P], m1 = sm.am1[ob * NP1 + P];
-                const float v0 = sm.s2[oa * NP1 + P], v1 = sm.s2[ob * NP1 + P];
-                const float a0 = (m0 == lg) ? v0 : 0.0f;
-                const float a1 = (vb && m1 == lg) ? v1 : 0.0f;
-                c[0] = mfma(a0, bx, c[0]);
-                c[1] = mfma(a1, bx, c[1]);
-            };
-            int P = wave;
-            for (; P + NW < NP1; P += 2 * NW) {
-                step(P, acc[0]);
-                step(P + NW, acc[1]);
-            }
-            if (P < NP1) step(P, acc[0]);
-            float *red = sm.pushbuf[0];  // [wavefront][tile][lane][4]
+            // operands of four positions (P0 + NW u) read at once, then their
+            // selects and matrix instructions; the bias gradients are summed
+            // from the same operands (per lane over its positions, then over
+            // the lane groups and, after the barrier, the wavefronts in order)
+            float bsum[2] = {0.0f, 0.0f};
+            for (int P0 = wave; P0 < NP1; P0 += 4 * NW) {
+                float bx[4], v0[4], v1[4];
+                int m0[4], m1[4];
 #pragma unroll
-            for (int t = 0; t < 2; ++t)
+                for (int u = 0; u < 4; ++u) {
+                    const int P = (P0 + NW * u < NP1) ? P0 + NW * u : NP1 - 1;
+                    const int py = P / Q1, px = P - py * Q1;
+                    bx[u] = sm.x[2 * py * IN + 2 * px + xo];
+                    // both reads unconditional (ob is 0 when the map is past C1)
+                    m0[u] = sm.am1[oa * NP1 + P];
+                    m1[u] = sm.am1[ob * NP1 + P];
+                    v0[u] = sm.s2[oa * NP1 + P];
+                    v1[u] = sm.s2[ob * NP1 + P];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (P0 + NW * u < NP1) {
+                        const float a0 = (m0[u] == lg) ? v0[u] : 0.0f;
+                        const float a1 = (vb && m1[u] == lg) ? v1[u] : 0.0f;
+                        acc[u & 1][0] = mfma(a0, bx[u], acc[u & 1][0]);
+                        acc[u & 1][1] = mfma(a1, bx[u], acc[u & 1][1]);
+                        bsum[0] += a0;
+                        bsum[1] += a1;
+                    }
+                }
+            }
+            float *red = sm.pushbuf[0];  // [wavefront][tile][lane][4], then [wavefront][32] bias sums
+            float *redb = red + NW * 2 * 256;
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
                 *(f4 *)(red + ((wave * 2 + t) * 64 + lane) * 4) = acc[0][t] + acc[1][t];
+                const float b1 = bsum[t] + __shfl_xor(bsum[t], 16, 64);
+                const float b2 = b1 + __shfl_xor(b1, 32, 64);
+                if (lg == 0) redb[wave * 32 + 16 * t + lr] = b2;
+            }
+            static_assert(NW * (2 * 256 + 32) <= NW * 16 * 65, "conv1 partial tiles and bias sums fit the push buffer");
             __syncthreads();
             for (int t = tid; t < C1 * 16 + C1; t += NT) {
                 if (t < C1 * 16) {
@@ -1041,10 +1070,10 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     push(DW1 + t, OW1 + t, g);
                 } else {
                     const int o = t - C1 * 16;
-                    float g4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-                    for (int q = 0; q < NP1; ++q) g4[q & 3] += sm.s2[o * NP1 + q];
-                    push(DB1 + o, OB1 + o, (g4[0] + g4[1]) + (g4[2] + g4[3]));
+                    float g = redb[o];
+#pragma unroll
+                    for (int w = 1; w < NW; ++w) g += redb[w * 32 + o];
+                    push(DB1 + o, OB1 + o, g);
                 }
             }
         }
