@@ -249,6 +249,7 @@ def worker_sweep(chaos, wl, torch):
             rows.append({"workers": w, "samples": n, "samples_per_s": sps,
                          "tflops": sps * flops / 1e12,
                          "kernel": "fused" if w <= net.max_workers else "one-wavefront generic"})
+            print(f"sweep {name}: {w} workers, {sps:,.0f} samples/s", file=sys.stderr, flush=True)
         out[name] = {"max_workers": net.max_workers, "worker_limit": net.worker_limit,
                      "train_flop_per_sample": flops, "points": rows}
     return {"sweep": "Hogwild training throughput vs concurrent workers", "nets": out}
