@@ -299,7 +299,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                     for (int j = 0; j < S::CT1; ++j) acc[q][j] = f4{0.f, 0.f, 0.f, 0.f};
                 }
                 // the pass's 24 inputs are read at once, ahead of the matrix
-                // instructions (selects after the scheduling barrier)
+                // instructions
                 float xv[4][6];
 #pragma unroll
                 for (int s = 0; s < 4; ++s)
@@ -735,7 +735,7 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         // pool2 backward -> dense conv2 deltas: a thread per pooled output
         // writes its whole 3x3 window (the delta at the first maximum, zeros
         // elsewhere; the windows tile the 9x9 map); the buffer's padding
-        // (positions 81..95 of every map, maps C2..C2P-1) is zeroed apart.
+        // (positions 81..D2S-1 of every map, maps C2..C2P-1) is zeroed apart.
         // Then clear e1.
         for (int q = tid; q < S::NF1; q += NT) {
             const int o = q / S::NP2, P = q - o * S::NP2, py = P / 3, px = P - 3 * py;

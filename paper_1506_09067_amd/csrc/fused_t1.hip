@@ -910,7 +910,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     for (int q = 0; q < NTT; ++q) acc[i][q] = mfma(a, bv[q], acc[i][q]);
                 }
             };
-            // KPOS positions per iteration: all their reads first, then their
+            // kT1Pos positions per iteration: all their reads first, then their
             // matrix instructions in position order, each waiting for its own
             // position's reads (no read crosses the loop's back edge, where
             // the register allocator's copies would wait for all of them)
