@@ -598,32 +598,51 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                     xv[c] = (i < NF1) ? sm.p3[i] : 0.0f;
                     ep[c] = 0.0f;
                 }
-                // FC1_ROWS rows per step: 15 FC1_ROWS pushes in flight before
-                // their returns are used (a wavefront's rows are still summed
-                // in increasing order)
-                for (int j = wave; j < F1; j += FC1_ROWS * NW) {
-                    float old[FC1_ROWS][15], dr[FC1_ROWS];
+                // The wavefront's rows j = wave + NW r (r < 38) in half-steps
+                // of FC1_ROWS / 2 rows: the next half-step's pushes are issued
+                // before the current one's returns are summed, so about
+                // 15 FC1_ROWS pushes stay in flight throughout (a row is summed
+                // once all its returns are in, rows in increasing order).
+                constexpr int HR = FC1_ROWS / 2, NR = (F1 + NW - 1) / NW;
+                static_assert(NR % (2 * HR) == HR, "38 rows: pairs of half-steps and a last half-step");
+                float oldA[HR][15], oldB[HR][15];
+                auto issue = [&](float (&o)[HR][15], int r0) {
 #pragma unroll
-                    for (int r = 0; r < FC1_ROWS; ++r) {
-                        const int jr = j + r * NW;
-                        dr[r] = (jr < F1) ? sm.dh[jr] : 0.0f;
-                        if (jr < F1) {
+                    for (int r = 0; r < HR; ++r) {
+                        const int jr = wave + NW * (r0 + r);
+                        const float d = (jr < F1) ? sm.dh[jr] : 0.0f;
 #pragma unroll
-                            for (int c = 0; c < 15; ++c) {
-                                int i = lane + 64 * c;
-                                old[r][c] = (i < NF1) ? push.with_old(DF1 + jr * NF1S + i, OF1 + jr * NF1 + i, dr[r] * xv[c])
-                                                      : 0.0f;
-                            }
-                        } else {
-#pragma unroll
-                            for (int c = 0; c < 15; ++c) old[r][c] = 0.0f;
+                        for (int c = 0; c < 15; ++c) {
+                            const int i = lane + 64 * c;
+                            o[r][c] = (jr < F1 && i < NF1) ? push.with_old(DF1 + jr * NF1S + i, OF1 + jr * NF1 + i, d * xv[c])
+                                                           : 0.0f;
                         }
                     }
+                };
+                auto consume = [&](const float (&o)[HR][15], int r0) {
 #pragma unroll
-                    for (int r = 0; r < FC1_ROWS; ++r)
+                    for (int r = 0; r < HR; ++r) {
+                        const int jr = wave + NW * (r0 + r);
+                        const float d = (jr < F1) ? sm.dh[jr] : 0.0f;
 #pragma unroll
-                        for (int c = 0; c < 15; ++c) ep[c] = fmaf(old[r][c], dr[r], ep[c]);
+                        for (int c = 0; c < 15; ++c) ep[c] = fmaf(o[r][c], d, ep[c]);
+                    }
+                };
+                // (scheduling barriers keep the half-steps in this order)
+                issue(oldA, 0);
+#pragma unroll 1
+                for (int r0 = 0; r0 + 2 * HR < NR; r0 += 2 * HR) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    issue(oldB, r0 + HR);
+                    __builtin_amdgcn_sched_barrier(0);
+                    consume(oldA, r0);
+                    __builtin_amdgcn_sched_barrier(0);
+                    issue(oldA, r0 + 2 * HR);
+                    __builtin_amdgcn_sched_barrier(0);
+                    consume(oldB, r0 + HR);
                 }
+                __builtin_amdgcn_sched_barrier(0);
+                consume(oldA, NR - HR);
                 float *part = sm.pushbuf[0];  // [wavefront][input]
 #pragma unroll
                 for (int c = 0; c < 15; ++c) {
