@@ -697,32 +697,61 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                 xv[c] = (i < S::NF1) ? sm.p2[i] : 0.0f;
                 ep[c] = 0.0f;
             }
-            // R rows per step: IC * R returning pushes in flight before their
-            // returns are used (a wavefront's rows are still summed in
-            // increasing order)
-            constexpr int R = (64 / IC < 16) ? 64 / IC : 16;
-            for (int j = wave; j < S::F1; j += R * NW) {
-                float old[R][IC], dr[R];
+            // The wavefront's rows j = wave + NW r in half-steps of HR rows
+            // (IC HR returning pushes each): the next half-step's pushes are
+            // issued before the current one's returns are summed, so about
+            // 2 IC HR stay in flight throughout (a row is summed once all its
+            // returns are in, rows in increasing order; scheduling barriers
+            // keep the half-steps in this order).
+            constexpr int R = (64 / IC < 16) ? 64 / IC : 16, HR = R / 2;
+            constexpr int NR = (S::F1 + NW - 1) / NW, NH = (NR + HR - 1) / HR;
+            static_assert(HR >= 1 && NH >= 2, "at least two half-steps");
+            float oA[HR][IC], oB[HR][IC];
+            auto issue = [&](float (&o)[HR][IC], int r0) {
 #pragma unroll
-                for (int r = 0; r < R; ++r) {
-                    const int jr = j + r * NW;
-                    dr[r] = (jr < S::F1) ? sm.dh[jr] : 0.0f;
-                    if (jr < S::F1) {
+                for (int r = 0; r < HR; ++r) {
+                    const int jr = wave + NW * (r0 + r);
+                    const float d = (jr < S::F1) ? sm.dh[jr] : 0.0f;
 #pragma unroll
-                        for (int c = 0; c < IC; ++c) {
-                            int i = lane + 64 * c;
-                            old[r][c] = (i < S::NF1) ? push_now.with_old(S::DF1 + jr * S::NF1S + i, S::OF1 + jr * S::NF1 + i, dr[r] * xv[c])
-                                                     : 0.0f;
-                        }
-                    } else {
-#pragma unroll
-                        for (int c = 0; c < IC; ++c) old[r][c] = 0.0f;
+                    for (int c = 0; c < IC; ++c) {
+                        const int i = lane + 64 * c;
+                        o[r][c] = (jr < S::F1 && i < S::NF1)
+                                      ? push_now.with_old(S::DF1 + jr * S::NF1S + i, S::OF1 + jr * S::NF1 + i, d * xv[c])
+                                      : 0.0f;
                     }
                 }
+            };
+            auto consume = [&](const float (&o)[HR][IC], int r0) {
 #pragma unroll
-                for (int r = 0; r < R; ++r)
+                for (int r = 0; r < HR; ++r) {
+                    const int jr = wave + NW * (r0 + r);
+                    const float d = (jr < S::F1) ? sm.dh[jr] : 0.0f;
 #pragma unroll
-                    for (int c = 0; c < IC; ++c) ep[c] = fmaf(old[r][c], dr[r], ep[c]);
+                    for (int c = 0; c < IC; ++c) ep[c] = fmaf(o[r][c], d, ep[c]);
+                }
+            };
+            issue(oA, 0);
+            int h = 0;
+#pragma unroll 1
+            for (; h + 2 < NH; h += 2) {
+                __builtin_amdgcn_sched_barrier(0);
+                issue(oB, (h + 1) * HR);
+                __builtin_amdgcn_sched_barrier(0);
+                consume(oA, h * HR);
+                __builtin_amdgcn_sched_barrier(0);
+                issue(oA, (h + 2) * HR);
+                __builtin_amdgcn_sched_barrier(0);
+                consume(oB, (h + 1) * HR);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if constexpr (NH % 2 == 0) {
+                issue(oB, (NH - 1) * HR);
+                __builtin_amdgcn_sched_barrier(0);
+                consume(oA, (NH - 2) * HR);
+                __builtin_amdgcn_sched_barrier(0);
+                consume(oB, (NH - 1) * HR);
+            } else {
+                consume(oA, (NH - 1) * HR);
             }
 #pragma unroll
             for (int c = 0; c < IC; ++c) {
