@@ -161,7 +161,7 @@ __device__ void fc_wgrad(const Layer &ly, const float *__restrict__ in,
 }
 
 template <int MODE>
-__global__ void __launch_bounds__(256) worker_kernel(Net net, WorkArgs a) {
+__global__ void __launch_bounds__(256, 8) worker_kernel(Net net, WorkArgs a) {
     __shared__ int64_t s_idx;
     __shared__ float s_red[4];
     float *ws = a.scratch + (int64_t)blockIdx.x * net.scratch_floats;
