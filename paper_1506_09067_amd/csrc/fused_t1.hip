@@ -224,37 +224,48 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
 #pragma unroll
             for (int i = 0; i < M2T; ++i) acc[i] = f4{0.f, 0.f, 0.f, 0.f};
             // weights: unconditional 16-byte loads (the address is in bounds
-            // for every lane), zeroed by a select where the lane's k or map is
-            // past the end, so no branch separates a load from its use
-            auto load = [&](int S) {
-                const f4 v = *(const f4 *)(wrow + 16 * S);
-                const bool ok = ov && 16 * S + 4 * lg < KC2;
-                return f4{ok ? v.x : 0.f, ok ? v.y : 0.f, ok ? v.z : 0.f, ok ? v.w : 0.f};
-            };
-            // A operands of sub-step (S, e) for every row tile; the next
-            // sub-step's are read while this one's matrix instructions run
-            float aC[M2T], aN[M2T];
-            auto read_a = [&](float (&av)[M2T], int off) {
+            // for every lane: padding maps read map 0, whose accumulators are
+            // never used).  The zeroing of K padding (k >= 500) is a select
+            // at the use, three super-steps later: a select at the load would
+            // make the load wait for its data at once.
+            auto load = [&](int S) { return *(const f4 *)(wrow + 16 * S); };
+            // A operands of a sub-step for every row tile, in two buffers:
+            // sub-step e multiplies buffer e % 2 and reads the next sub-step's
+            // operands into the other one, each read issued right after the
+            // matrix instruction of the same row tile (held there by
+            // scheduling barriers).  A read is then consumed a whole sub-step
+            // (31 matrix instructions) after it was issued, and no wait for an
+            // operand waits for a read issued since.
+            float a0[M2T], a1v[M2T];
+            auto sub = [&](const float (&cur)[M2T], float (&nxt)[M2T], float bk, int offn) {
 #pragma unroll
-                for (int i = 0; i < M2T; ++i) av[i] = sm.a1[base[i] + off];
+                for (int i = 0; i < M2T; ++i) {
+                    acc[i] = mfma(cur[i], bk, acc[i]);
+                    __builtin_amdgcn_sched_barrier(0);
+                    nxt[i] = sm.a1[base[i] + offn];
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             };
-            auto step = [&](f4 b, int S) {
+            // one super-step: buffer a0 holds its first sub-step's operands on
+            // entry and the next super-step's first on exit
+            auto step = [&](f4 raw, int S) {
                 const int4 ko = *(const int4 *)(sm.koff2 + 16 * S + 4 * lg);
                 const int4 kn = *(const int4 *)(sm.koff2 + 16 * (S + 1 < KC2P / 16 ? S + 1 : S) + 4 * lg);
-                const int offs[5] = {ko.x, ko.y, ko.z, ko.w, kn.x};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    read_a(aN, offs[e + 1]);
-#pragma unroll
-                    for (int i = 0; i < M2T; ++i) acc[i] = mfma(aC[i], b[e], acc[i]);
-#pragma unroll
-                    for (int i = 0; i < M2T; ++i) aC[i] = aN[i];
-                }
+                const bool ok = 16 * S + 4 * lg < KC2;
+                const f4 b = f4{ok ? raw.x : 0.f, ok ? raw.y : 0.f, ok ? raw.z : 0.f, ok ? raw.w : 0.f};
+                sub(a0, a1v, b[0], ko.y);
+                sub(a1v, a0, b[1], ko.z);
+                sub(a0, a1v, b[2], ko.w);
+                sub(a1v, a0, b[3], kn.x);
             };
             constexpr int NS = KC2P / 16;  // 32 super-steps, a ring of four weight buffers
             static_assert(NS % 4 == 0, "whole rounds");
             f4 b0 = load(0), b1 = load(1), b2 = load(2), b3;
-            read_a(aC, sm.koff2[4 * lg]);
+            {
+                const int off0 = sm.koff2[4 * lg];
+#pragma unroll
+                for (int i = 0; i < M2T; ++i) a0[i] = sm.a1[base[i] + off0];
+            }
             for (int S = 0; S < NS; S += 4) {
                 b3 = load(S + 3);
                 step(b0, S);
