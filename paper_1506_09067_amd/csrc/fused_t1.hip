@@ -101,6 +101,7 @@ struct alignas(16) Smem {
     alignas(16) int koff2[KC2P];         // im2col offset into a1 of k = (c,u,v), conv2 (0 past KC2)
     unsigned char am3[NF1 + 4];          // pool2 argmax
     float sink[128];                     // scatter target of padding lanes
+    float b3s[C3];                       // conv3 biases (copied in the conv3 forward)
     int64_t idx;
 };
 static_assert(sizeof(Smem) <= 160 * 1024, "LDS budget");
@@ -213,6 +214,8 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
             const int o = 16 * wave + lr;
             const bool ov = o < C2;
             const float *wrow = W + DW2 + (ov ? o : 0) * KC2S + 4 * lg;
+            // the bias, requested now so that the epilogue does not wait for it
+            const float bias2 = W[DB2 + (ov ? o : 0)];
             int base[M2T];
 #pragma unroll
             for (int i = 0; i < M2T; ++i) {
@@ -277,7 +280,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 step(b3, S + 3);
             }
             if (ov) {
-                const float bias = W[DB2 + o];
+                const float bias = bias2;
 #pragma unroll
                 for (int i = 0; i < M2T; ++i) {
                     const int P = 4 * i + lg;
@@ -337,9 +340,13 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                         for (int j = 0; j < 7; ++j) acc[i][j] = mfma(av[i], b[j][s], acc[i][j]);
                 }
             };
+            // the biases, requested with the first weights and kept in LDS for
+            // the epilogue (read there, they would cost it a round trip)
+            const float b3pre = W[DB3 + (tid < C3 ? tid : C3 - 1)];
             // weights two super-steps ahead (a ring of three buffers)
             load_b(bA, S0);
             if (S0 + 1 < S1) load_b(bB, S0 + 1);
+            if (tid < C3) sm.b3s[tid] = b3pre;
             for (int S = S0; S < S1; S += 3) {
                 if (S + 2 < S1) load_b(bC, S + 2);
                 compute(bA, S);
@@ -389,7 +396,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     if ((j >= 4) != (wave == 1)) continue;
                     int o = 16 * j + lr;
                     if (o >= C3) continue;
-                    float bias = W[DB3 + o];
+                    float bias = sm.b3s[o];
 #pragma unroll
                     for (int i = 0; i < 3; ++i) {
                         f4 t = acc[i][j] + *(const f4 *)(buf + ((i * 7 + j) * 64 + lane) * 4);
@@ -422,6 +429,9 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 xin[c] = (i < NF1) ? *(const f4 *)(sm.p3 + i) : f4{0.f, 0.f, 0.f, 0.f};
             }
             const int jb = 38 * wave, je = (jb + 38 < F1) ? jb + 38 : F1;
+            // lane l holds the bias of row jb + l, requested with the first
+            // rows' weights
+            const float bfx = W[DBF1 + (jb + lane < F1 ? jb + lane : F1 - 1)];
             f4 wv[8][4];
             auto load_rows = [&](int j0) {
 #pragma unroll
@@ -462,21 +472,41 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 t1 += __shfl_xor(t1, 2, 64);
                 t1 += __shfl_xor(t1, 1, 64);
                 const int j = j0 + ((lane >> 3) & 7);
-                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + W[DBF1 + j]);
+                const float bias = __shfl(bfx, (j - jb) & 63, 64);
+                if ((lane & 7) == 0 && j < je) sm.h[j] = act_y(t1 + bias);
             }
         }
         __syncthreads();
-        // FC2 (output layer)
-        for (int j = wave; j < F2; j += NW) {
-            const float *wj = W + DF2 + j * F1S;
-            float s = 0.0f;
+        // FC2 (output layer): wavefront w computes outputs w, w + 4, w + 8;
+        // all their weights and biases are requested before the first is used
+        // (every load is used unconditionally, a padding lane multiplying a
+        // zero, so none is moved into a branch where it would be waited for
+        // at once)
+        {
+            float wf[3][3], bf[3];
 #pragma unroll
-            for (int it = 0; it < 3; ++it) {
-                int i = lane + 64 * it;
-                if (i < F1) s = fmaf(wj[i], sm.h[i], s);
+            for (int q = 0; q < 3; ++q) {
+                const int j = (wave + NW * q < F2) ? wave + NW * q : F2 - 1;
+#pragma unroll
+                for (int it = 0; it < 3; ++it) {
+                    const int i = lane + 64 * it;
+                    wf[q][it] = W[DF2 + j * F1S + (i < F1 ? i : 0)];
+                }
+                bf[q] = W[DBF2 + j];
             }
-            s = wave_sum(s);
-            if (lane == 0) sm.o[j] = act_y(s + W[DBF2 + j]);
+#pragma unroll
+            for (int q = 0; q < 3; ++q) {
+                const int j = wave + NW * q;
+                if (j >= F2) break;
+                float s = 0.0f;
+#pragma unroll
+                for (int it = 0; it < 3; ++it) {
+                    const int i = lane + 64 * it;
+                    s = fmaf(wf[q][it], (i < F1) ? sm.h[i < F1 ? i : 0] : 0.0f, s);
+                }
+                s = wave_sum(s);
+                if (lane == 0) sm.o[j] = act_y(s + bf[q]);
+            }
         }
         __syncthreads();
         if (a.out && tid < F2) a.out[idx * F2 + tid] = sm.o[tid];
