@@ -194,10 +194,15 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
 #pragma unroll
                         for (int j = 0; j < 2; ++j) {
                             int o = 16 * j + lr;
-                            if (o < C1) sm.a1[o * NA1 + m] = act_y(acc[q][j][r] + b1[j]);
+                            if (o < C1) sm.a1[o * NA1 + m] = acc[q][j][r] + b1[j];
                         }
                     }
             }
+            // the activation over the 13,520 outputs, one per thread in turn
+            // (applied in the tile epilogue, the lanes of map tile 1 past map
+            // 19 would idle through it)
+            __syncthreads();
+            for (int t = tid; t < C1 * NA1; t += NT) sm.a1[t] = act_y(sm.a1[t]);
         };
 
         // ================= forward propagation =================
