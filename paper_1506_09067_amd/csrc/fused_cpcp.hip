@@ -445,26 +445,6 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         }
         __syncthreads();
 
-        // ---- pool2: 3x3 windows of the 9x9 maps, first maximum wins.  y2
-        //      holds the conv2 outputs before the activation; f is strictly
-        //      increasing, so the window's maximum is taken on z and f is
-        //      applied to it alone. ----
-        for (int t = tid; t < S::NF1; t += NT) {
-            int o = t / S::NP2, P = t - o * S::NP2;
-            int py = P / 3, px = P - 3 * py;
-            const float *zo = sm.y2 + o * S::NY2 + 3 * py * S::H2 + 3 * px;
-            float m = zo[0];
-            int ag = 0;
-#pragma unroll
-            for (int w = 1; w < 9; ++w) {
-                float v = zo[(w / 3) * S::H2 + (w % 3)];
-                if (v > m) { m = v; ag = w; }
-            }
-            sm.p2[t] = act_y(m);
-            sm.am2[t] = (unsigned char)ag;
-        }
-        __syncthreads();
-
         // ---- FC1: wavefront w computes neurons [JW w, JW w + JW), eight at a
         //      time, lanes over the inputs (16-byte loads when the rows are
         //      16-byte aligned); the eight partial sums of a lane are reduced
@@ -474,14 +454,6 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
         {
             constexpr int VEC = S::FC1_VEC, IC = (S::NF1 + 64 * VEC - 1) / (64 * VEC);
             constexpr int JW = (S::F1 + NW - 1) / NW;
-            float xin[IC][VEC];
-#pragma unroll
-            for (int c = 0; c < IC; ++c)
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) {
-                    int i = VEC * lane + 64 * VEC * c + e;
-                    xin[c][e] = (i < S::NF1) ? sm.p2[i] : 0.0f;
-                }
             const int jb = JW * wave, je = (jb + JW < S::F1) ? jb + JW : S::F1;
             float wv[8][IC][VEC];
             auto load_rows = [&](int j0) {
@@ -501,8 +473,38 @@ __global__ void __launch_bounds__(NT, MINB) fused_cpcp_kernel(WorkArgs a) {
                         }
                     }
             };
-            const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
+            // the first rows are requested before the pool2 phase, whose
+            // maxima and the barrier after it then hide part of their wait
             if (jb < je) load_rows(jb);
+            // ---- pool2: 3x3 windows of the 9x9 maps, first maximum wins.  y2
+            //      holds the conv2 outputs before the activation; f is strictly
+            //      increasing, so the window's maximum is taken on z and f is
+            //      applied to it alone. ----
+            for (int t = tid; t < S::NF1; t += NT) {
+                int o = t / S::NP2, P = t - o * S::NP2;
+                int py = P / 3, px = P - 3 * py;
+                const float *zo = sm.y2 + o * S::NY2 + 3 * py * S::H2 + 3 * px;
+                float m = zo[0];
+                int ag = 0;
+#pragma unroll
+                for (int w = 1; w < 9; ++w) {
+                    float v = zo[(w / 3) * S::H2 + (w % 3)];
+                    if (v > m) { m = v; ag = w; }
+                }
+                sm.p2[t] = act_y(m);
+                sm.am2[t] = (unsigned char)ag;
+            }
+            __syncthreads();
+
+            float xin[IC][VEC];
+#pragma unroll
+            for (int c = 0; c < IC; ++c)
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) {
+                    int i = VEC * lane + 64 * VEC * c + e;
+                    xin[c][e] = (i < S::NF1) ? sm.p2[i] : 0.0f;
+                }
+            const bool b5 = lane & 32, b4 = lane & 16, b3 = lane & 8;
             for (int j0 = jb; j0 < je; j0 += 8) {
                 float sq[8];
 #pragma unroll
