@@ -156,16 +156,18 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         // o < 20, K = 16; a wavefront's tiles i = wave + 4q, six at a time.
         // Also used to recompute the output for the conv2 weight gradient.
         auto conv1_forward = [&]() {
+            // unconditional loads (padding maps read map 19 into outputs that
+            // are never stored): a select at a load makes it wait at once
             float bw[4][2], b1[2];
 #pragma unroll
             for (int s = 0; s < 4; ++s)
 #pragma unroll
                 for (int j = 0; j < 2; ++j) {
-                    int o = 16 * j + lr;
-                    bw[s][j] = (o < C1) ? W[DW1 + o * 16 + 4 * s + lg] : 0.0f;
+                    const int o = 16 * j + lr;
+                    bw[s][j] = W[DW1 + (o < C1 ? o : C1 - 1) * 16 + 4 * s + lg];
                 }
 #pragma unroll
-            for (int j = 0; j < 2; ++j) b1[j] = (16 * j + lr < C1) ? W[DB1 + 16 * j + lr] : 0.0f;
+            for (int j = 0; j < 2; ++j) b1[j] = W[DB1 + (16 * j + lr < C1 ? 16 * j + lr : C1 - 1)];
             for (int i0 = wave; i0 < 43; i0 += 6 * NW) {
                 f4 acc[6][2];
                 int base[6];
