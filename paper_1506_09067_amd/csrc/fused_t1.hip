@@ -336,16 +336,20 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
             auto compute = [&](const f4 (&b)[7], int S) {
                 const int4 ko = *(const int4 *)(sm.koff3 + 16 * S + 4 * lg);
                 const int offs[4] = {ko.x, ko.y, ko.z, ko.w};
+                // the super-step's twelve activations are read at once: the
+                // later sub-steps' arrive while the first one computes
+                float av[4][3];
 #pragma unroll
-                for (int s = 0; s < 4; ++s) {
-                    float av[3];
+                for (int s = 0; s < 4; ++s)
 #pragma unroll
-                    for (int i = 0; i < 3; ++i) av[i] = sm.y2[base[i] + offs[s]];  // padding rows: unused
+                    for (int i = 0; i < 3; ++i) av[s][i] = sm.y2[base[i] + offs[s]];  // padding rows: unused
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int s = 0; s < 4; ++s)
 #pragma unroll
                     for (int i = 0; i < 3; ++i)
 #pragma unroll
-                        for (int j = 0; j < 7; ++j) acc[i][j] = mfma(av[i], b[j][s], acc[i][j]);
-                }
+                        for (int j = 0; j < 7; ++j) acc[i][j] = mfma(av[s][i], b[j][s], acc[i][j]);
             };
             // the biases, requested with the first weights and kept in LDS for
             // the epilogue (read there, they would cost it a round trip)
