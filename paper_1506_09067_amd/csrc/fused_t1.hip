@@ -779,18 +779,23 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 }
                 const int k4 = 64 * grp + lane;
                 const float *y4 = sm.y2 + (k4 < KC3 ? sm.koff3[k4] : 0);
+                // the group's 36 activations are read at once: later steps'
+                // arrive while the first ones compute
+                float bv[18][2];
 #pragma unroll
                 for (int ms = 0; ms < 18; ++ms) {
                     const int m = 2 * ms + (lane >> 5), wp = window_pos(m >> 2, m & 3, 3, H2);
-                    float bv[2];
 #pragma unroll
-                    for (int kt = 0; kt < 2; ++kt) bv[kt] = y32[kt][wp];
+                    for (int kt = 0; kt < 2; ++kt) bv[ms][kt] = y32[kt][wp];
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int ms = 0; ms < 18; ++ms)
 #pragma unroll
                     for (int i = 0; i < 3; ++i)
 #pragma unroll
                         for (int kt = 0; kt < 2; ++kt)
-                            c32[i][kt] = mfma32(a32[i][ms], bv[kt], ms == 0 ? f16{} : c32[i][kt]);
-                }
+                            c32[i][kt] = mfma32(a32[i][ms], bv[ms][kt], ms == 0 ? f16{} : c32[i][kt]);
                 // two partial sums (even and odd m) keep the chain short
 #pragma unroll
                 for (int m = 0; m < M3; ++m) {
