@@ -81,7 +81,7 @@ struct alignas(16) Smem {
         float red3[2 * 21 * 256];        // conv3 split-K partial sums (forward)
         struct {
             float s2[C2 * NY2];          // conv3 backward-data sums
-            float d3[C3 * M3P];          // conv3 output deltas, rows (P, w)
+            alignas(16) float d3[C3 * M3P];  // conv3 output deltas, rows (P, w)
         };
         float red1[NW * 2 * 256];        // conv1 partial gradient tiles
     };
@@ -678,14 +678,20 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 sm.e3[q] = ((part[q] + part[NF1 + q]) + part[2 * NF1 + q]) + part[3 * NF1 + q];
             __syncthreads();
         }
-        for (int t = tid; t < C3 * M3P; t += NT) {
-            int o = t / M3P, m = t - o * M3P;
-            float d = 0.0f;
-            if (m < M3) {
-                int P = m >> 2, w = m & 3, q = o * NP3 + P;
-                if (sm.am3[q] == w) d = sm.e3[q] * dact_from_y(sm.p3[q]);
-            }
-            sm.d3[t] = d;
+        // (a thread per pooled output writes its window's four deltas, rows
+        // 4P..4P+3 of its map, as one 16-byte store: the delta at the first
+        // maximum, zeros elsewhere; rows M3..M3P-1 of every map are zeroed apart)
+#pragma unroll 1
+        for (int q = tid; q < NF1; q += NT) {
+            const int o = q / NP3, P = q - o * NP3, ag = sm.am3[q];
+            const float d = sm.e3[q] * dact_from_y(sm.p3[q]);
+            *(f4 *)(sm.d3 + o * M3P + 4 * P) = f4{ag == 0 ? d : 0.0f, ag == 1 ? d : 0.0f, ag == 2 ? d : 0.0f,
+                                                  ag == 3 ? d : 0.0f};
+        }
+        static_assert(M3 % 4 == 0 && M3P % 4 == 0 && (C2 * NY2) % 4 == 0, "16-byte delta rows");
+        for (int t = tid; t < C3 * (M3P - M3) / 4; t += NT) {
+            const int o = t / ((M3P - M3) / 4), r = t - o * ((M3P - M3) / 4);
+            *(f4 *)(sm.d3 + o * M3P + M3 + 4 * r) = f4{0.f, 0.f, 0.f, 0.f};
         }
         for (int t = tid; t < C2 * NY2; t += NT) sm.s2[t] = 0.0f;
         __syncthreads();
@@ -705,7 +711,7 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 for (int j = 0; j < 3; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
             const int k0 = blk * 144;
             const int arow = k0 + (lr >> 2) * 36 + (lr & 3);
-            float aA[9], aB[9], bA[3], bB[3];
+            float aA[9], aB[9], aC[9], bA[3], bB[3], bC[3];
             auto load = [&](float (&av)[9], float (&bv)[3], int ks) {
                 const float *w3 = W + DW3 + (4 * ks + lg) * KC3 + arow;
 #pragma unroll
@@ -715,20 +721,29 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 for (int j = 0; j < 3; ++j) bv[j] = dd[16 * j];
             };
             auto compute = [&](const float (&av)[9], const float (&bv)[3]) {
+                // keeps the weight reads of the steps ahead issued before
+                // these matrix instructions wait for this step's
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int i = 0; i < 9; ++i)
 #pragma unroll
                     for (int j = 0; j < 3; ++j) acc[i][j] = mfma(av[i], bv[j], acc[i][j]);
             };
-            // the next output maps' weights and deltas are loaded while the
-            // current ones compute
+            // weights and deltas two output-map steps ahead (a ring of three
+            // buffers)
+            constexpr int NKS = C3 / 4;
             load(aA, bA, 0);
-            for (int ks = 0; ks < C3 / 4; ks += 2) {
-                if (ks + 1 < C3 / 4) load(aB, bB, ks + 1);
+            load(aB, bB, 1);
+            for (int ks = 0; ks < NKS; ks += 3) {
+                if (ks + 2 < NKS) load(aC, bC, ks + 2);
                 compute(aA, bA);
-                if (ks + 1 < C3 / 4) {
-                    if (ks + 2 < C3 / 4) load(aA, bA, ks + 2);
+                if (ks + 1 < NKS) {
+                    if (ks + 3 < NKS) load(aA, bA, ks + 3);
                     compute(aB, bB);
+                }
+                if (ks + 2 < NKS) {
+                    if (ks + 4 < NKS) load(aB, bB, ks + 4);
+                    compute(aC, bC);
                 }
             }
             float *dst = sm.s2 + (4 * blk + lg) * NY2;
