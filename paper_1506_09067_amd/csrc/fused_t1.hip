@@ -122,6 +122,10 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         sm.koff2[k] = (k < KC2) ? c * NA1 + u * H1 + v : 0;
     }
 
+    // Training: thread 0 claims the worker's next sample as soon as the
+    // current one is known (Section III-A.1), so the claim's round trip to
+    // the shared counter overlaps a whole sample instead of starting it.
+    int next = -1;
     for (int64_t step = 0;; ++step) {
         // opaque thread index: keeps per-phase index arithmetic inside its phase
         int tid_l = threadIdx.x;
@@ -130,9 +134,10 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         const int wave = __builtin_amdgcn_readfirstlane(tid_l >> 6);
         // ---- claim a sample (Section III-A.1) ----
         if (tid == 0) {
-            if (kTrain && step == 0 && blockIdx.x > 0)
+            if (kTrain && next < 0 && blockIdx.x > 0)
                 join_after(a.counter, a.n, (int)blockIdx.x / kJoinRamp);
-            sm.idx = kTrain ? (int64_t)atomicAdd(a.counter, 1) : (int64_t)blockIdx.x + step * gridDim.x;
+            if (kTrain) sm.idx = (next >= 0) ? next : atomicAdd(a.counter, 1);
+            else sm.idx = (int64_t)blockIdx.x + step * gridDim.x;
         }
         // Reads are on demand.  Every wavefront first waits for its own
         // pushes of the previous sample to complete (the worker sees its own
@@ -145,8 +150,9 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         __syncthreads();
         const int64_t idx = sm.idx;
         if (idx >= a.n) break;
-        if (kTrain) {
-            if (a.claims && tid == 0) atomicAdd(a.claims + idx, 1);
+        if (kTrain && tid == 0) {
+            next = atomicAdd(a.counter, 1);
+            if (a.claims) atomicAdd(a.claims + idx, 1);
         }
         const int label = a.labels[idx];
         for (int i = tid; i < NX; i += NT) sm.x[i] = a.x[idx * NX + i];
