@@ -210,7 +210,16 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
             // (applied in the tile epilogue, the lanes of map tile 1 past map
             // 19 would idle through it)
             __syncthreads();
-            for (int t = tid; t < C1 * NA1; t += NT) sm.a1[t] = act_y(sm.a1[t]);
+            // four outputs per thread and round: their reads are issued
+            // together, so the LDS round trip is paid once per four
+            static_assert(C1 * NA1 % 4 == 0, "whole rounds of four");
+            for (int t0 = tid; t0 < C1 * NA1 / 4; t0 += NT) {
+                float v[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) v[q] = sm.a1[t0 + q * (C1 * NA1 / 4)];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) sm.a1[t0 + q * (C1 * NA1 / 4)] = act_y(v[q]);
+            }
         };
 
         // ================= forward propagation =================
