@@ -91,7 +91,7 @@ struct alignas(16) Smem {
             alignas(16) float e3[NF1];   // dE/d(pool2 output)
             float fcpart[NW * NF1];      // FC1 backward partial sums per wavefront
         };
-        float e1[C1 * NA1];              // dE/d(conv1 output), then conv1 deltas
+        alignas(16) float e1[C1 * NA1];  // dE/d(conv1 output), then conv1 deltas
     };
     float y2[C2 * NY2];                  // pooled conv2 output (conv3 input), then its deltas
     unsigned char am2[C2 * NY2 + 4];     // pool after conv2: argmax (window element 0..3)
@@ -863,8 +863,19 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         // conv2 deltas at the pooled positions (in place of y2); the delta of a
         // conv2 output off its window's maximum is zero.  Clear the conv1
         // error buffer.
-        for (int t = tid; t < C2 * NY2; t += NT) sm.y2[t] = sm.s2[t] * dact_from_y(sm.y2[t]);
-        for (int t = tid; t < C1 * NA1; t += NT) sm.e1[t] = 0.0f;
+        // (four elements per thread and round: their reads are issued together)
+        static_assert(C2 * NY2 % 4 == 0 && C1 * NA1 % 4 == 0, "whole rounds of four");
+        for (int t0 = tid; t0 < C2 * NY2 / 4; t0 += NT) {
+            float e[4], y[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                e[q] = sm.s2[t0 + q * (C2 * NY2 / 4)];
+                y[q] = sm.y2[t0 + q * (C2 * NY2 / 4)];
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) sm.y2[t0 + q * (C2 * NY2 / 4)] = e[q] * dact_from_y(y[q]);
+        }
+        for (int t = tid; t < C1 * NA1 / 4; t += NT) *(f4 *)(sm.e1 + 4 * t) = f4{0.f, 0.f, 0.f, 0.f};
         __syncthreads();
         // the conv1 output again (its region held the conv3 buffers meanwhile)
         conv1_forward();
@@ -1050,7 +1061,16 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         }
         __syncthreads();
         // conv1 deltas: e1 * f'(conv1 output)
-        for (int t = tid; t < C1 * NA1; t += NT) sm.e1[t] *= dact_from_y(sm.a1[t]);
+        for (int t0 = tid; t0 < C1 * NA1 / 4; t0 += NT) {
+            float e[4], y[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                e[q] = sm.e1[t0 + q * (C1 * NA1 / 4)];
+                y[q] = sm.a1[t0 + q * (C1 * NA1 / 4)];
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) sm.e1[t0 + q * (C1 * NA1 / 4)] = e[q] * dact_from_y(y[q]);
+        }
         __syncthreads();
 
         // conv1 weight gradient G[o][uv] = sum over the 676 outputs of the
