@@ -852,9 +852,20 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
         __syncthreads();
 
         // conv2 deltas (in place of y2) and clear the pool1 error buffer
-        for (int t = tid; t < C2 * NY2; t += NT) {
-            sm.y2[t] = sm.s2[t] * dact_from_y(sm.y2[t]);
-            sm.s2[t] = 0.0f;
+        // (four elements per thread and round: their reads are issued together)
+        static_assert(C2 * NY2 % 4 == 0, "whole rounds of four");
+        for (int t0 = tid; t0 < C2 * NY2 / 4; t0 += NT) {
+            float e[4], y[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                e[q] = sm.s2[t0 + q * (C2 * NY2 / 4)];
+                y[q] = sm.y2[t0 + q * (C2 * NY2 / 4)];
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                sm.y2[t0 + q * (C2 * NY2 / 4)] = e[q] * dact_from_y(y[q]);
+                sm.s2[t0 + q * (C2 * NY2 / 4)] = 0.0f;
+            }
         }
         __syncthreads();
 
@@ -1018,7 +1029,17 @@ __global__ void __launch_bounds__(NT, 1) fused_large_kernel(WorkArgs a) {
                 for (int p = 0; p < NY2; ++p) g4[p & 3] += sm.y2[tid * NY2 + p];
                 push(DB2 + tid, OB2 + tid, (g4[0] + g4[1]) + (g4[2] + g4[3]));
             }
-            for (int t = tid; t < C1 * NP1; t += NT) sm.s2[t] *= dact_from_y(sm.p1[t]);
+            static_assert(C1 * NP1 % 4 == 0, "whole rounds of four");
+            for (int t0 = tid; t0 < C1 * NP1 / 4; t0 += NT) {
+                float e[4], y[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    e[q] = sm.s2[t0 + q * (C1 * NP1 / 4)];
+                    y[q] = sm.p1[t0 + q * (C1 * NP1 / 4)];
+                }
+#pragma unroll
+                for (int q = 0; q < 4; ++q) sm.s2[t0 + q * (C1 * NP1 / 4)] = e[q] * dact_from_y(y[q]);
+            }
         }
         __syncthreads();
 
