@@ -68,8 +68,9 @@ constexpr int FC1_ROWS = 4;  // FC1 rows a wavefront pushes per step (returning 
 // fifth backward-data block) and of wavefronts 1 and 2 (wavefront 3 takes the
 // rest of the 32)
 constexpr int kT1W0 = 3, kT1W = 10;
-// pooled positions whose operands the weight gradient reads at once
-constexpr int kT1Pos = 6;
+// pooled positions whose operands the weight gradient reads at once (121 =
+// 11 x 11: no partial batch)
+constexpr int kT1Pos = 11;
 
 // conv3 output rows m = 4 * P + w (P pooled 3x3 position, w window element)
 constexpr int M3 = 36, M3P = 48;                // padded to 3 tiles of 16
