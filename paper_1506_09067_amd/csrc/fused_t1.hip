@@ -67,7 +67,7 @@ constexpr int FC1_ROWS = 4;  // FC1 rows a wavefront pushes per step (returning 
 // conv2 weight-gradient column tiles of wavefront 0 (which also takes the
 // fifth backward-data block) and of wavefronts 1 and 2 (wavefront 3 takes the
 // rest of the 32)
-constexpr int kT1W0 = 3, kT1W = 10;
+constexpr int kT1W0 = 2, kT1W = 10;
 // pooled positions whose operands the weight gradient reads at once (121 =
 // 11 x 11: no partial batch)
 constexpr int kT1Pos = 11;
@@ -886,8 +886,8 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         // inputs and write different outputs, in one phase so that the work
         // can be balanced over the wavefronts: backward data comes in 5 blocks
         // of 4 input maps (wavefront w takes block w, wavefront 0 also block
-        // 4), the weight gradient in 32 column tiles (wavefront 0 takes 3,
-        // the others 10, 10 and 9).
+        // 4), the weight gradient in 32 column tiles (wavefront 0 takes 2,
+        // the others 10 each).
         //
         // Backward data: C[k][m] = sum_o W2[o][k] d2[o][m], k = (c,u,v),
         // col2im into e1[c][pos(m) + (u,v)].  Row q of tile i holds map
