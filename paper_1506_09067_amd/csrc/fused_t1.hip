@@ -781,7 +781,10 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                     scatter_add<3>(dm, u * H2 + v, c);
                 }
         }
-        __syncthreads();
+        // (no barrier: the weight gradient below reads what the backward data
+        // reads and writes elsewhere, so each wavefront goes on with it; the
+        // 15 backward-data blocks leave wavefront 3 one block short, which
+        // takes two more column groups: 10 against 8)
 
         // conv3 weight gradient G[o][k] = sum_m d3[o][m] y2col[m][k], pushed.
         // Maps 0..95 on 32x32x2 tiles: element r of a tile holds maps
@@ -789,8 +792,9 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
         // instruction writes two 128-byte runs of weights.  Maps 96..99 on
         // the 16-block 4x4x1 instruction with block b, column c at
         // k = 4b + c: element r holds map 96 + r at 64 consecutive k.
-        // Wavefront w takes the 64-column groups w, w + 4, ... (a column
-        // beyond KC3 computes values never pushed).
+        // Wavefront 3 takes the 64-column groups 0..9, wavefront w < 3 the
+        // groups 10 + 8w .. 17 + 8w (a column beyond KC3 computes values
+        // never pushed).
         {
             float a32[3][18];  // A[o = 32i + l%32][m = 2ms + l/32]
 #pragma unroll
@@ -799,7 +803,9 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
                 for (int ms = 0; ms < 18; ++ms)
                     a32[i][ms] = sm.d3[(32 * i + (lane & 31)) * M3P + 2 * ms + (lane >> 5)];
             const float *a4 = sm.d3 + (96 + (lane & 3)) * M3P;  // A[block][l%4][m]: map 96 + l%4
-            for (int grp = wave; grp < (KC3 / 16 + 3) / 4; grp += NW) {
+            static_assert((KC3 / 16 + 3) / 4 == 34 && C2 / 4 == 15, "34 column groups, 15 backward-data blocks");
+            const int g0 = (wave == 3) ? 0 : 10 + 8 * wave, g1 = (wave == 3) ? 10 : g0 + 8;
+            for (int grp = g0; grp < g1; ++grp) {
                 f16 c32[3][2];
                 f4 c4[2];
                 const float *y32[2];
