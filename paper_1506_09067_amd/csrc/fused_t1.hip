@@ -1007,27 +1007,43 @@ __global__ void __launch_bounds__(NT, 1) fused_t1_kernel(WorkArgs a) {
 #pragma unroll
                 for (int q = 0; q < NTT; ++q) bv[q] = sm.a1[base + ko[q]];
             };
-            auto compute = [&](const int (&am)[4], const float (&av)[4], const float (&bv)[NTT]) {
+            // the A operands of a position: each row tile's pooled delta
+            // where this lane group's window element is the maximum
+            auto select = [&](const int (&am)[4], const float (&av)[4], float (&as)[4]) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float a = (ovv[i] && am[i] == lg) ? av[i] : 0.0f;
-#pragma unroll
-                    for (int q = 0; q < NTT; ++q) acc[i][q] = mfma(a, bv[q], acc[i][q]);
-                }
+                for (int i = 0; i < 4; ++i) as[i] = (ovv[i] && am[i] == lg) ? av[i] : 0.0f;
             };
             // kT1Pos positions per iteration: all their reads first, then their
-            // matrix instructions in position order, each waiting for its own
-            // position's reads (no read crosses the loop's back edge, where
-            // the register allocator's copies would wait for all of them)
+            // matrix instructions in position order (no read crosses the
+            // loop's back edge, where the register allocator's copies would
+            // wait for all of them).  A position's selects are formed under
+            // the previous position's matrix instructions, into registers
+            // that no instruction still in the matrix pipeline reads: a
+            // select that rewrites the operand of the instruction just issued
+            // waits for that instruction to read it.
+            static_assert(NY2 % kT1Pos == 0, "whole batches of positions");
             for (int P0 = 0; P0 < NY2; P0 += kT1Pos) {
                 int am[kT1Pos][4];
-                float av[kT1Pos][4], bv[kT1Pos][NTT];
+                float av[kT1Pos][4], bv[kT1Pos][NTT], as[kT1Pos][4];
 #pragma unroll
-                for (int u = 0; u < kT1Pos; ++u) operands(P0 + u < NY2 ? P0 + u : NY2 - 1, am[u], av[u], bv[u]);
+                for (int u = 0; u < kT1Pos; ++u) operands(P0 + u, am[u], av[u], bv[u]);
                 __builtin_amdgcn_sched_barrier(0);
+                select(am[0], av[0], as[0]);
 #pragma unroll
                 for (int u = 0; u < kT1Pos; ++u)
-                    if (P0 + u < NY2) compute(am[u], av[u], bv[u]);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int q = 0; q < NTT; ++q) acc[i][q] = mfma(as[u][i], bv[u][q], acc[i][q]);
+                        if (i == 1 && u + 1 < kT1Pos) {
+                            __builtin_amdgcn_sched_barrier(0);
+                            select(am[u + 1], av[u + 1], as[u + 1]);
+                            // the operand just issued stays live across the
+                            // selects, so none of them is given its register
+                            asm volatile("" ::"v"(as[u][1]));
+                        }
+                    }
             }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
